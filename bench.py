@@ -1,0 +1,161 @@
+"""Benchmark: GPT-2 124M FP32 training step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--batch 16] [--no-cpu-baseline]
+
+One step = bt_gpt2_train_step: forward, backward, global-norm clip and AdamW
+over all 124,475,904 parameters, B x T = 16 x 1024 tokens of a seeded Zipf
+stream (a stand-in for the paper's FineWeb-Edu corpus), random-init weights
+of the paper's initialisation.  Inputs are resident in HBM before timing.
+
+Prints one JSON line: tokens/s over the K timed steps (HIP events on the
+library's stream, synchronised on both sides), the live roofline of the
+dominant kernel class (the FP32 MFMA GEMMs) from the step profiler's events
+over the same timed region, a per-class breakdown, and the float64 CPU oracle
+timed on a bounded sample of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+MFMA_FP32_PEAK_TFLOPS = 157.3   # MI355X dense FP32 matrix peak
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E peak
+PAPER_1GPU_TOKS = 54600         # paper, 1 GPU eager (RTX 6000 Ada): context only
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--batch", type=int, default=16)
+    ap.add_argument("--seq", type=int, default=1024)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-tokens", type=int, default=1024)
+    return ap.parse_args()
+
+
+def cpu_baseline(sample_tokens: int):
+    """The float64 oracle, as it stands, on a bounded sample of the same
+    workload: one full step (fwd + bwd + clip + AdamW over all parameters)
+    of the 124M model on `sample_tokens` tokens of the same stream."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    from oracle import gpt2 as og
+    from paper_2606_24780_amd import synth
+
+    cfg, hp = synth.GPT2_124M, synth.HP_124M
+    specs = synth.param_specs(cfg)
+    params = synth.init_params(cfg, 4)
+    T = min(cfg.max_T, sample_tokens)
+    B = max(1, sample_tokens // T)
+    stream = synth.zipf_tokens(B * T + 1, cfg.V, 1.1, 40)
+    x, y = synth.shifted_pair(stream, B, T)
+    zeros = {k: np.zeros(s, dtype=np.float64) for k, s, _ in specs}
+    t0 = time.perf_counter()
+    og.train_step(cfg, hp, specs, params, zeros, zeros, x, y, t=1)
+    dt = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    return {"value": B * T / dt, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"one full float64 step (fwd+bwd+clip+AdamW over all 124.5M params) of GPT-2 124M on "
+                      f"{B}x{T} tokens of the benchmark's token stream; {dt:.1f} s wall",
+            "seconds": dt, "host_cpus": os.cpu_count()}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(f"bench.py: only --gpus 1 is supported by this build (got {a.gpus}); "
+              "the multi-GPU data-parallel exchange is not implemented", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2606_24780_amd import bt, synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    cfg, hp = synth.GPT2_124M, synth.HP_124M
+    B, T = a.batch, a.seq
+    params = synth.init_params(cfg, 4)
+    stream = synth.zipf_tokens(B * T + 1, cfg.V, 1.1, 40)
+    x, y = synth.shifted_pair(stream, B, T)
+    torch.cuda.reset_peak_memory_stats()
+    model = bt.GPT2(cfg, hp, B, T)
+    model.load_params(synth.flatten(cfg, params))
+    xd = torch.from_numpy(x).cuda()
+    yd = torch.from_numpy(y).cuda()
+    torch.cuda.synchronize()
+
+    for _ in range(a.warmup):
+        model.train_step(xd, yd)
+    torch.cuda.synchronize()
+
+    model.profile_enable(True)
+    model.profile_read(reset=True)
+    s = model.stream
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    ev0.record(s)
+    losses = []
+    for _ in range(a.steps):
+        losses.append(model.train_step(xd, yd))
+    ev1.record(s)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    ms = ev0.elapsed_time(ev1)
+    prof = model.profile_read(reset=True)
+    model.profile_enable(False)
+
+    tok_s = a.steps * B * T / (ms / 1e3)
+    g = prof["gemm"]
+    gemm_tflops = g["flops"] / (g["ms"] / 1e3) / 1e12 if g["ms"] > 0 else 0.0
+    kernels = {}
+    for name, st in prof.items():
+        if st["launches"] == 0:
+            continue
+        k = {"calls_per_step": st["launches"] / a.steps, "ms_per_step": st["ms"] / a.steps}
+        if st["flops"] > 0 and name in ("gemm", "attn_fwd", "attn_bwd"):
+            k["tflops"] = st["flops"] / (st["ms"] / 1e3) / 1e12
+            k["frac_mfma_fp32"] = k["tflops"] / MFMA_FP32_PEAK_TFLOPS
+        if st["bytes"] > 0 and name not in ("gemm", "attn_fwd", "attn_bwd"):
+            k["gbs"] = st["bytes"] / (st["ms"] / 1e3) / 1e9
+            k["frac_hbm"] = k["gbs"] / HBM_PEAK_GBS
+        kernels[name] = k
+    roofline = {
+        "kernel": "gemm_f32_mfma (all bt_gemm calls of the step, incl. split-K reduction)",
+        "bound": "mfma", "achieved": round(gemm_tflops, 3), "peak": MFMA_FP32_PEAK_TFLOPS,
+        "unit": "TFLOP/s", "frac": round(gemm_tflops / MFMA_FP32_PEAK_TFLOPS, 4), "traffic": None,
+        "launches": g["launches"], "avg_launch_ms": g["ms"] / max(1, g["launches"]),
+        "flops_per_launch": g["flops"] / max(1, g["launches"]),
+    }
+    out = {
+        "metric": "GPT-2 124M FP32 train tokens/s on 1 GPU; GEMM fraction of FP32 MFMA peak",
+        "value": round(tok_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": round(ms / a.steps, 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "GPT-2 124M FP32 train step (fwd+bwd+clip+AdamW), one GPU's data-parallel shard",
+                   "batch": B, "seq_len": T, "layers": cfg.L, "d_model": cfg.C, "heads": cfg.H,
+                   "vocab": cfg.V, "vocab_padded": cfg.Vp, "params": model.P,
+                   "tokens": "Zipf(1.1) synthetic stream, seed 40; params seed 4"},
+        "roofline": roofline,
+        "kernels": kernels,
+        "wall_s": round(wall, 3),
+        "loss_first_last": [losses[0], losses[-1]],
+        "peak_mem_gib": round(torch.cuda.max_memory_allocated() / 2**30, 2),
+        "paper_context_tokens_s": PAPER_1GPU_TOKS,
+    }
+    if not a.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(a.cpu_sample_tokens)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

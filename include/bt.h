@@ -1,0 +1,326 @@
+/*
+ * bt.h -- C ABI of libbt, an MI355X (gfx950) implementation of one FP32 GPT-2
+ * training step on one GPU's data-parallel shard.
+ *
+ * The operations follow the paper's statement of the problem: the layer
+ * definitions, every forward and backward operator and the AdamW step of a
+ * GPT-2 decoder (Evaluation section: GPT-2 architecture figure caption and
+ * the "Training hyperparameters" table), the per-kernel list of the
+ * "Performance Benchmarks" appendix (attention, GELU, LayerNorm, sparse
+ * cross-entropy, reduce-sum, AdamW), the dense projections served by the
+ * native GEMM library ("Implementation", native GEMM library paragraph) and
+ * the micro-step loop of Algorithm "Distributed Data Parallel Training Step".
+ *
+ * Conventions for every entry point
+ *  - Pointers are DEVICE pointers unless a comment says "host".  All floating
+ *    point tensors are FP32, row-major, contiguous unless a leading dimension
+ *    is given.  Integer tensors are int32.
+ *  - The caller owns every buffer.  libbt never allocates, frees or keeps
+ *    device memory; scratch space is passed in as a workspace (ws) whose size
+ *    is given by the matching *_ws_bytes query.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  All
+ *    work is enqueued asynchronously on it; only bt_gpt2_train_step blocks
+ *    the host (once, to return the loss).
+ *  - Arguments are validated before anything is launched.  On a violation a
+ *    BT_E* code is returned, nothing is launched and bt_last_error() gives a
+ *    thread-local detail string.  A failed launch returns BT_EHIP.
+ *  - Alignment: every float pointer must be 16-byte aligned; leading
+ *    dimensions and the dimensions named "vectorised" must be multiples of 4.
+ *  - Results are deterministic: no floating-point atomics, fixed-order
+ *    reductions, so identical calls give bitwise identical results.
+ */
+#ifndef BT_H
+#define BT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  BT_OK = 0,
+  BT_EINVAL = 1,      /* NULL pointer or out-of-range scalar argument */
+  BT_ESHAPE = 2,      /* inconsistent or unsupported shape */
+  BT_EALIGN = 3,      /* pointer or leading dimension not suitably aligned */
+  BT_EWORKSPACE = 4,  /* workspace missing or smaller than the query says */
+  BT_EHIP = 5,        /* a HIP runtime call or kernel launch failed */
+  BT_ENONFINITE = 6   /* reserved: non-finite value detected on the host */
+} bt_status;
+
+const char* bt_status_str(bt_status s);
+/* Detail string of the last non-OK status returned on this host thread. */
+const char* bt_last_error(void);
+/* Library version, "major.minor.patch". */
+const char* bt_version(void);
+
+typedef enum { BT_OP_N = 0, BT_OP_T = 1 } bt_op;
+
+typedef enum {
+  BT_EPI_NONE = 0,      /* out = acc */
+  BT_EPI_BIAS = 1,      /* out = acc + bias[n] */
+  BT_EPI_BIAS_GELU = 2, /* pre = acc + bias[n]; optional preact_out = pre; out = gelu(pre) */
+  BT_EPI_DGELU = 3      /* out = acc * gelu'(gelu_in[m, n])  (GELU backward fused) */
+} bt_epi;
+
+/*
+ * Dense product (native GEMM library paragraph of "Implementation": QKV,
+ * attention-output and MLP projections in forward and backward layouts).
+ *
+ *   C[m, n] = epi( sum_k op(A)[m, k] * op(B)[k, n] ) + residual[m, n] + beta * C[m, n]
+ *
+ * op(A) is A (M x K, lda >= K) for BT_OP_N or A^T with A stored K x M
+ * (lda >= M) for BT_OP_T; likewise op(B) is B (K x N, ldb >= N) or B^T with
+ * B stored N x K (ldb >= K).  C is M x N with ldc >= N.  beta is 0 or 1
+ * (1 = accumulate into C, used for gradient accumulation).
+ * bias [N] is required for BIAS / BIAS_GELU.  preact_out (M x N, ldc) is
+ * optional for BIAS_GELU.  gelu_in (M x N, ldc) is required for DGELU.
+ * residual (M x N, ldc) is optional and must not alias C.
+ * M, N, K >= 0 (an empty product writes beta*C + residual with acc = 0; with
+ * K = 0 the epilogue still applies).  M, N, K, lda, ldb, ldc must be
+ * multiples of 4.  FP32 inputs, FP32 accumulation on the matrix cores.
+ * ws may be NULL when bt_gemm_ws_bytes() returns 0 for the shape; otherwise
+ * it must hold that many bytes (split-K partial products).
+ */
+bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K,
+                  const float* A, int lda, const float* B, int ldb,
+                  float beta, float* C, int ldc,
+                  const float* bias, bt_epi epi, float* preact_out, const float* gelu_in,
+                  const float* residual, void* ws, size_t ws_bytes, void* stream);
+size_t bt_gemm_ws_bytes(bt_op opA, bt_op opB, int M, int N, int K, bt_epi epi);
+
+/*
+ * Causal multi-head self-attention forward (GPT-2 architecture figure:
+ * masked multi-head self-attention; appendix "Attention Forward", causal
+ * case).  Per batch b and head h: S = Q K^T / sqrt(hd) with key j visible to
+ * query i iff j <= i, P = softmax(S) row-wise, O = P V.
+ *   qkv [B, T, 3, H, hd]   (the QKV projection output, [B*T, 3*H*hd])
+ *   out [B, T, H, hd]      (written)
+ *   lse [B, H, T]          (written; natural-log sum of exp of each score row)
+ * hd a multiple of 4, at most 64 (heads below 32 are zero-padded to 32
+ * inside the kernel).  T >= 1, B, H >= 1.  qkv and out 16-byte aligned.
+ */
+bt_status bt_attention_fwd(const float* qkv, float* out, float* lse,
+                           int B, int T, int H, int hd, void* stream);
+
+/*
+ * Causal attention backward (appendix "Attention Backward").  From dout
+ * [B, T, H, hd], qkv, out and lse of the forward it writes dqkv [B, T, 3, H,
+ * hd] (overwritten).  P is recomputed from lse.  ws holds
+ * bt_attention_bwd_ws_bytes() bytes (row sums of dout * out).
+ */
+bt_status bt_attention_bwd(const float* dout, const float* qkv, const float* out,
+                           const float* lse, float* dqkv, void* ws, size_t ws_bytes,
+                           int B, int T, int H, int hd, void* stream);
+size_t bt_attention_bwd_ws_bytes(int B, int T, int H, int hd);
+
+/*
+ * LayerNorm forward over the last dimension (pre-normalised blocks of the
+ * GPT-2 architecture figure; appendix "LayerNorm Forward"):
+ *   mean = sum_c x / C, var = sum_c (x - mean)^2 / C, rstd = 1/sqrt(var + eps)
+ *   y = gamma * (x - mean) * rstd + beta
+ * x, y [M, C]; mean, rstd [M] (written, for the backward).  C multiple of 4,
+ * C <= 4096.  y must not alias x.
+ */
+bt_status bt_layernorm_fwd(const float* x, const float* gamma, const float* beta,
+                           float* y, float* mean, float* rstd, int M, int C, float eps,
+                           void* stream);
+
+/*
+ * LayerNorm backward (appendix "LayerNorm Backward").  With
+ * xhat = (x - mean) * rstd and g = dy * gamma:
+ *   dx     = dx_beta * dx + rstd * (g - mean_c(g) - xhat * mean_c(g * xhat))
+ *   dgamma = param_beta * dgamma + sum_m dy * xhat
+ *   dbeta  = param_beta * dbeta  + sum_m dy
+ * dx_beta, param_beta in {0, 1}.  dx may alias dy only when dx_beta == 0.
+ * ws holds bt_layernorm_bwd_ws_bytes(M, C) bytes (per-block column partials,
+ * reduced in a fixed order).
+ */
+bt_status bt_layernorm_bwd(const float* dy, const float* x, const float* gamma,
+                           const float* mean, const float* rstd, float* dx, float* dgamma,
+                           float* dbeta, float dx_beta, float param_beta, void* ws,
+                           size_t ws_bytes, int M, int C, void* stream);
+size_t bt_layernorm_bwd_ws_bytes(int M, int C);
+
+/*
+ * tanh-form GELU (GPT-2 figure: GELU feed-forward sublayer; appendix "GELU
+ * Forward / Backward"):  gelu(x) = x/2 (1 + tanh(sqrt(2/pi)(x + 0.044715 x^3))).
+ * bt_gelu_fwd: y = gelu(x).  bt_gelu_bwd: dx = dy * gelu'(x); dx may alias dy.
+ * n must be a multiple of 4.
+ */
+bt_status bt_gelu_fwd(const float* x, float* y, size_t n, void* stream);
+bt_status bt_gelu_bwd(const float* x, const float* dy, float* dx, size_t n, void* stream);
+
+/*
+ * Sparse (integer-target) softmax cross-entropy over the first V of Vp
+ * columns (Algorithm "Distributed Data Parallel Training Step": cross-entropy
+ * of the forward against the target; appendix "Sparse Cross-Entropy Loss").
+ *   lse[m]       = log sum_{j<V} exp(z[m, j])
+ *   loss_rows[m] = lse[m] - z[m, targets[m]]
+ * targets in [0, V).  Vp multiple of 4, V <= Vp.  Out-of-range targets give
+ * BT_EINVAL only if detected on the host; on the device they are clamped and
+ * the row's loss is set to NaN.
+ */
+bt_status bt_softmax_xent_fwd(const float* logits, const int32_t* targets, float* loss_rows,
+                              float* lse, int M, int V, int Vp, void* stream);
+/* dlogits[m, j] = (exp(z[m, j] - lse[m]) - [j == targets[m]]) * scale for j < V, 0 for
+ * j >= V.  dlogits may alias logits (in place). */
+bt_status bt_softmax_xent_bwd(const float* logits, const float* lse, const int32_t* targets,
+                              float* dlogits, float scale, int M, int V, int Vp, void* stream);
+/* Fused forward + backward in one pass over each row: writes loss_rows and lse
+ * and overwrites logits with dlogits (scale as above). */
+bt_status bt_softmax_xent_fused(float* logits, const int32_t* targets, float* loss_rows,
+                                float* lse, float scale, int M, int V, int Vp, void* stream);
+
+/*
+ * AdamW over one flat arena, one launch ("Implementation: Horizontal Tensor
+ * Fusion"; hyper-parameter table).  For every element i < n, with
+ * c = *grad_scale (1 if grad_scale is NULL) and d = (i < n_decay):
+ *   g = c * g[i];  m = b1 m + (1-b1) g;  v = b2 v + (1-b2) g^2
+ *   p = p - lr*wd*d*p - lr * (m / (1-b1^t)) / (sqrt(v / (1-b2^t)) + eps)
+ * t >= 1.  n and n_decay multiples of 4, n_decay <= n.
+ */
+bt_status bt_adamw_step(float* p, const float* g, float* m, float* v, size_t n, size_t n_decay,
+                        float lr, float beta1, float beta2, float eps, float weight_decay, int t,
+                        const float* grad_scale, void* stream);
+
+/*
+ * Global gradient-norm clip (hyper-parameter table: gradient clip 1.0):
+ *   norm = sqrt(sum_i g[i]^2);  coef = min(1, clip / (norm + 1e-6))  (coef = 1 if clip <= 0)
+ * Writes the two device scalars out_norm[0], out_coef[0].  Fixed-order
+ * two-stage reduction.  ws holds bt_grad_norm_ws_bytes(n) bytes.  n multiple of 4.
+ */
+bt_status bt_grad_norm_clip(const float* g, size_t n, float clip, float* out_norm,
+                            float* out_coef, void* ws, size_t ws_bytes, void* stream);
+size_t bt_grad_norm_ws_bytes(size_t n);
+
+/*
+ * Embeddings with learned positions and the token table tied to the LM head
+ * (GPT-2 architecture figure).  tokens [B, T] in [0, Vp).
+ * fwd: x0[b, t, :] = wte[tokens[b, t], :] + wpe[t, :]            (x0 [B*T, C])
+ * bwd: dwte[v, :] += sum over positions with token v of dx0       (always accumulates)
+ *      dwpe[t, :]  = wpe_beta * dwpe[t, :] + sum_b dx0[b, t, :]    (rows t < T)
+ * The backward sorts positions by token on the device and sums each token's
+ * rows in position order (deterministic).  ws holds
+ * bt_embedding_bwd_ws_bytes(B, T, C, Vp) bytes.  C multiple of 4.
+ */
+bt_status bt_embedding_fwd(const int32_t* tokens, const float* wte, const float* wpe, float* x0,
+                           int B, int T, int C, int Vp, void* stream);
+bt_status bt_embedding_bwd(const int32_t* tokens, const float* dx0, float* dwte, float* dwpe,
+                           float wpe_beta, void* ws, size_t ws_bytes, int B, int T, int C, int Vp,
+                           void* stream);
+size_t bt_embedding_bwd_ws_bytes(int B, int T, int C, int Vp);
+
+/*
+ * Column sums ("reduce-sum" kernel of the appendix; bias gradients):
+ *   out[n] = beta * out[n] + sum_m X[m, n]      (X [M, N], ldx >= N)
+ * Fixed-order two-stage reduction.  ws holds bt_colsum_ws_bytes(M, N) bytes.
+ */
+bt_status bt_colsum(const float* X, int M, int N, int ldx, float* out, float beta, void* ws,
+                    size_t ws_bytes, void* stream);
+size_t bt_colsum_ws_bytes(int M, int N);
+
+/* ------------------------------------------------------------------------
+ * Composed GPT-2 step.
+ *
+ * Flat parameter layout (also the layout of grads, m and v), decayed prefix
+ * first:  wte [Vp, C], wpe [max_T, C], then for each layer l: Wqkv [C, 3C],
+ * Wo [C, C], Wfc [C, 4C], Wfp [4C, C]  (linear weights stored [in, out]);
+ * then, not decayed, for each layer: ln1g [C], ln1b [C], bqkv [3C], bo [C],
+ * ln2g [C], ln2b [C], bfc [4C], bfp [C]; then lnfg [C], lnfb [C].
+ * opt_state is [m | v], 2 * P floats.
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int V;            /* real vocabulary (loss over columns < V) */
+  int Vp;           /* padded rows of wte (multiple of 4) */
+  int max_T;        /* rows of wpe */
+  int L;            /* layers */
+  int H;            /* heads; C / H must be 64 */
+  int C;            /* model width, multiple of 64 */
+  float ln_eps;     /* LayerNorm epsilon */
+  float lr, beta1, beta2, adam_eps, weight_decay;
+  float grad_clip;  /* <= 0: no clipping */
+} bt_gpt2_config;
+
+typedef struct bt_gpt2_ctx bt_gpt2_ctx;
+
+size_t bt_gpt2_num_params(const bt_gpt2_config* cfg);
+size_t bt_gpt2_num_decay_params(const bt_gpt2_config* cfg);
+/* offsets: host array of at least n_tensors+1 entries (call with offsets =
+ * NULL to get *n_tensors); entry i is the element offset of tensor i in the
+ * flat layout above, the last entry is P. */
+bt_status bt_gpt2_param_offsets(const bt_gpt2_config* cfg, size_t* offsets, int* n_tensors);
+/* Device workspace for activations and scratch of a step with up to
+ * max_B x max_T tokens. */
+size_t bt_gpt2_workspace_bytes(const bt_gpt2_config* cfg, int max_B, int max_T);
+/* Creates a host-side context bound to the caller's workspace and stream.
+ * The step counter t starts at 0. */
+bt_status bt_gpt2_create(const bt_gpt2_config* cfg, void* workspace, size_t ws_bytes, int max_B,
+                         int max_T, void* stream, bt_gpt2_ctx** out);
+/* Frees the host-side context only; never touches caller memory. */
+void bt_gpt2_destroy(bt_gpt2_ctx* ctx);
+/* Current step counter (number of optimizer steps taken). */
+int bt_gpt2_step_count(const bt_gpt2_ctx* ctx);
+void bt_gpt2_set_step_count(bt_gpt2_ctx* ctx, int t);
+
+/*
+ * Forward + backward of one micro-batch (Algorithm "Distributed Data Parallel
+ * Training Step", one micro-step).  Gradients are those of
+ * loss_scale * sum over the B*T positions of the per-position loss; they
+ * overwrite grads (accumulate = 0) or are added to it (accumulate = 1).
+ * d_loss (device scalar) receives loss_scale * sum of per-position losses,
+ * added to its previous value when accumulate = 1.  For one plain step use
+ * loss_scale = 1/(B*T); for k micro-steps 1/(B*T*k).  tokens, targets
+ * [B, T]; B <= max_B, T <= max_T of the context and T <= cfg.max_T.
+ * loss_rows (optional, device [B*T]) receives the unscaled per-position loss.
+ */
+bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, float* grads,
+                          const int32_t* tokens, const int32_t* targets, int B, int T,
+                          float loss_scale, int accumulate, float* d_loss, float* loss_rows);
+/* Global gradient norm, clip (cfg.grad_clip > 0) and AdamW at step t with
+ * learning rate lr.  The norm and clip coefficient stay on the device. */
+bt_status bt_gpt2_optimizer_step(bt_gpt2_ctx* ctx, float* params, float* grads, float* opt_state,
+                                 int t, float lr);
+/* Waits for the context's stream, then copies to host out[3] the device
+ * scalars [last loss written by bt_gpt2_train_step, gradient norm, clip
+ * coefficient] of the last step. */
+bt_status bt_gpt2_read_scalars(const bt_gpt2_ctx* ctx, float* out);
+
+/*
+ * Step profiler (the paper's kernel-level profiler, reduced to what this
+ * path needs).  When enabled, every kernel-class call made by
+ * bt_gpt2_fwd_bwd and bt_gpt2_optimizer_step is bracketed by two HIP events
+ * recorded on the context's stream; elapsed times and the algorithmic work
+ * of each call accumulate per class until read.  Event creation happens at
+ * enable time (host-side runtime objects; no device memory).
+ */
+enum {
+  BT_PROF_GEMM = 0, BT_PROF_ATTN_FWD, BT_PROF_ATTN_BWD, BT_PROF_LN_FWD, BT_PROF_LN_BWD,
+  BT_PROF_XENT, BT_PROF_EMB_FWD, BT_PROF_EMB_BWD, BT_PROF_COLSUM, BT_PROF_GRAD_NORM,
+  BT_PROF_ADAMW, BT_PROF_OTHER, BT_PROF_NCLASSES
+};
+typedef struct {
+  long long launches;  /* library calls of this class (one call may launch 2-3 kernels) */
+  double ms;           /* summed GPU time between the bracketing events */
+  double flops;        /* algorithmic floating-point operations */
+  double bytes;        /* algorithmic HBM bytes (each operand read / written once) */
+} bt_kernel_stat;
+bt_status bt_gpt2_profile_enable(bt_gpt2_ctx* ctx, int enable);
+/* Waits for the stream, then copies BT_PROF_NCLASSES entries to host out;
+ * reset != 0 clears the totals afterwards. */
+bt_status bt_gpt2_profile_read(bt_gpt2_ctx* ctx, bt_kernel_stat* out, int reset);
+
+/*
+ * One full training step: forward, backward, clip, AdamW (t = previous
+ * count + 1, lr = cfg.lr).  Returns the mean loss over the B*T positions at
+ * the pre-update parameters; NaN on error (see bt_last_error()).  Blocks
+ * until the step has finished.
+ */
+float bt_gpt2_train_step(bt_gpt2_ctx* ctx, float* params, float* grads, float* opt_state,
+                         const int32_t* tokens, const int32_t* targets, int B, int T);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* BT_H */

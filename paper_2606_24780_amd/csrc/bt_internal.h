@@ -1,0 +1,84 @@
+// Internal helpers shared by the libbt translation units (HIP, gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstddef>
+#include <cstdint>
+#include <cstdio>
+
+#include "../../include/bt.h"
+
+namespace bt {
+
+// Thread-local error detail; set_error returns the status so call sites can
+// `return fail(BT_ESHAPE, "...")`.
+bt_status fail(bt_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+void clear_error();
+
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// After a launch: turn a launch error into BT_EHIP.
+bt_status check_launch(const char* what);
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// Zero n floats with a small kernel (no memset node).
+bt_status fill_zero(float* p, size_t n, hipStream_t s);
+
+// ------------------------------------------------------------------ device
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// tanh-form GELU and its derivative (FP32).
+__device__ __forceinline__ float gelu_f(float x) {
+  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
+  const float k1 = 0.044715f;
+  float u = k0 * (x + k1 * x * x * x);
+  return 0.5f * x * (1.0f + tanhf(u));
+}
+
+__device__ __forceinline__ float gelu_grad_f(float x) {
+  const float k0 = 0.7978845608028654f;
+  const float k1 = 0.044715f;
+  float x2 = x * x;
+  float u = k0 * (x + k1 * x2 * x);
+  float t = tanhf(u);
+  float du = k0 * (1.0f + 3.0f * k1 * x2);
+  return 0.5f * (1.0f + t) + 0.5f * x * (1.0f - t * t) * du;
+}
+
+}  // namespace bt
+
+#define BT_CHECK_HIP(expr)                                                          \
+  do {                                                                              \
+    hipError_t _e = (expr);                                                         \
+    if (_e != hipSuccess)                                                           \
+      return ::bt::fail(BT_EHIP, "%s: %s", #expr, hipGetErrorString(_e));           \
+  } while (0)
+
+#define BT_RETURN_IF(cond, status, ...)                                             \
+  do {                                                                              \
+    if (cond) return ::bt::fail(status, __VA_ARGS__);                               \
+  } while (0)
+
+#define BT_TRY(expr)                                                                \
+  do {                                                                              \
+    bt_status _s = (expr);                                                          \
+    if (_s != BT_OK) return _s;                                                     \
+  } while (0)

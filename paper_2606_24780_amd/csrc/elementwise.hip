@@ -1,0 +1,293 @@
+// Memory-bound kernels: tanh-GELU forward/backward, the horizontally fused
+// AdamW update over the flat parameter arena, the global gradient norm and
+// clip coefficient, column sums (bias gradients) and the loss reduction.
+//
+// All are single-pass, float4 (global_load_dwordx4), grid-stride with about
+// 8 blocks of 256 threads per CU in flight; reductions are two-stage with a
+// fixed order, so results are bitwise reproducible.
+#include "bt_internal.h"
+
+namespace bt {
+namespace {
+
+constexpr int EW_THREADS = 256;
+
+unsigned ew_blocks(size_t n4) {
+  size_t nb = (n4 + EW_THREADS - 1) / EW_THREADS;
+  const size_t cap = 256 * 8;  // 8 blocks per CU on 256 CUs
+  if (nb > cap) nb = cap;
+  if (nb < 1) nb = 1;
+  return (unsigned)nb;
+}
+
+__global__ void __launch_bounds__(EW_THREADS) gelu_fwd_kernel(const floatx4* __restrict__ x,
+                                                              floatx4* __restrict__ y, size_t n4) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (size_t)gridDim.x * blockDim.x) {
+    floatx4 v = x[i], o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) o[k] = gelu_f(v[k]);
+    y[i] = o;
+  }
+}
+
+__global__ void __launch_bounds__(EW_THREADS) gelu_bwd_kernel(const floatx4* __restrict__ x, const floatx4* dy,
+                                                              floatx4* dx, size_t n4) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (size_t)gridDim.x * blockDim.x) {
+    floatx4 v = x[i], g = dy[i], o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) o[k] = g[k] * gelu_grad_f(v[k]);
+    dx[i] = o;
+  }
+}
+
+struct AdamArgs {
+  float lr, beta1, beta2, eps, wd;
+  float inv_bc1, inv_bc2;  // 1/(1-beta1^t), 1/(1-beta2^t)
+};
+
+__global__ void __launch_bounds__(EW_THREADS) adamw_kernel(floatx4* __restrict__ p, const floatx4* __restrict__ g,
+                                                           floatx4* __restrict__ m, floatx4* __restrict__ v,
+                                                           size_t n4, size_t nd4, AdamArgs a,
+                                                           const float* __restrict__ grad_scale) {
+  const float c = grad_scale ? *grad_scale : 1.f;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (size_t)gridDim.x * blockDim.x) {
+    floatx4 pp = p[i], gg = g[i], mm = m[i], vv = v[i];
+    const float dec = i < nd4 ? a.lr * a.wd : 0.f;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float gk = gg[k] * c;
+      mm[k] = a.beta1 * mm[k] + (1.f - a.beta1) * gk;
+      vv[k] = a.beta2 * vv[k] + (1.f - a.beta2) * gk * gk;
+      const float mhat = mm[k] * a.inv_bc1;
+      const float vhat = vv[k] * a.inv_bc2;
+      pp[k] = pp[k] - dec * pp[k] - a.lr * mhat / (sqrtf(vhat) + a.eps);
+    }
+    p[i] = pp;
+    m[i] = mm;
+    v[i] = vv;
+  }
+}
+
+// Block partial sums of squares in double (stage 1).
+__global__ void __launch_bounds__(EW_THREADS) sumsq_kernel(const floatx4* __restrict__ g, size_t n4,
+                                                           double* __restrict__ part) {
+  __shared__ double red[EW_THREADS / 64];
+  double s = 0.0;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (size_t)gridDim.x * blockDim.x) {
+    const floatx4 v = g[i];
+    s += (double)v[0] * v[0] + (double)v[1] * v[1] + (double)v[2] * v[2] + (double)v[3] * v[3];
+  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double t = 0.0;
+    for (int w = 0; w < EW_THREADS / 64; ++w) t += red[w];
+    part[blockIdx.x] = t;
+  }
+}
+
+// Stage 2: one block; fixed-order sum of partials, then norm and clip coef.
+__global__ void __launch_bounds__(EW_THREADS) norm_finish_kernel(const double* __restrict__ part, int nparts,
+                                                                 float clip, float* out_norm, float* out_coef) {
+  __shared__ double red[EW_THREADS];
+  double s = 0.0;
+  for (int i = threadIdx.x; i < nparts; i += blockDim.x) s += part[i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = EW_THREADS / 2; w >= 1; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const double norm = sqrt(red[0]);
+    double coef = 1.0;
+    if (clip > 0.f) {
+      coef = (double)clip / (norm + 1e-6);
+      if (coef > 1.0) coef = 1.0;
+    }
+    if (out_norm) *out_norm = (float)norm;
+    if (out_coef) *out_coef = (float)coef;
+  }
+}
+
+// Column sums, stage 1: block b sums rows [b*rpb, (b+1)*rpb) of every column.
+__global__ void __launch_bounds__(EW_THREADS) colsum_partial_kernel(const float* __restrict__ X, int M, int N,
+                                                                    long long ldx, int rpb,
+                                                                    float* __restrict__ part) {
+  const int N4 = N >> 2;
+  const int r0 = blockIdx.x * rpb;
+  const int r1 = min(M, r0 + rpb);
+  for (int c = threadIdx.x; c < N4; c += blockDim.x) {
+    floatx4 s = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int r = r0; r < r1; ++r) s += *reinterpret_cast<const floatx4*>(X + (long long)r * ldx + 4 * c);
+    *reinterpret_cast<floatx4*>(part + (long long)blockIdx.x * N + 4 * c) = s;
+  }
+}
+
+__global__ void __launch_bounds__(EW_THREADS) colsum_finish_kernel(const float* __restrict__ part, int nparts,
+                                                                   int N, float* __restrict__ out, float beta) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= N) return;
+  float s = 0.f;
+  for (int b = 0; b < nparts; ++b) s += part[(long long)b * N + c];
+  if (beta != 0.f) s += out[c];
+  out[c] = s;
+}
+
+int colsum_blocks(int M) {
+  int nb = (M + 31) / 32;
+  if (nb > 512) nb = 512;
+  if (nb < 1) nb = 1;
+  return nb;
+}
+
+}  // namespace
+
+// d_loss = acc * d_loss + scale * sum(rows)   (one block, fixed order, double)
+__global__ void __launch_bounds__(256) loss_sum_kernel(const float* __restrict__ rows, int n, float scale,
+                                                       int accumulate, float* d_loss) {
+  __shared__ double red[256];
+  double s = 0.0;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) s += rows[i];
+  red[threadIdx.x] = s;
+  __syncthreads();
+  for (int w = 128; w >= 1; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    const float v = (float)(red[0] * (double)scale);
+    *d_loss = accumulate ? *d_loss + v : v;
+  }
+}
+
+__global__ void __launch_bounds__(256) fill_zero_kernel(float* __restrict__ p, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = 0.f;
+}
+
+// Zero-fill with a kernel rather than a memset node, so the call is safe in
+// code that a caller captures into a HIP graph.
+bt_status fill_zero(float* p, size_t n, hipStream_t s) {
+  if (n == 0) return BT_OK;
+  size_t nb = (n + 255) / 256;
+  if (nb > 2048) nb = 2048;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((unsigned)nb), dim3(256), 0, s, p, n);
+  return check_launch("fill_zero_kernel");
+}
+
+bt_status launch_loss_sum(const float* rows, int n, float scale, int accumulate, float* d_loss, hipStream_t s) {
+  hipLaunchKernelGGL(loss_sum_kernel, dim3(1), dim3(256), 0, s, rows, n, scale, accumulate, d_loss);
+  return check_launch("loss_sum_kernel");
+}
+
+}  // namespace bt
+
+using namespace bt;
+
+extern "C" bt_status bt_gelu_fwd(const float* x, float* y, size_t n, void* stream) {
+  BT_RETURN_IF(n & 3, BT_ESHAPE, "bt_gelu_fwd: n=%zu must be a multiple of 4", n);
+  if (n == 0) return BT_OK;
+  BT_RETURN_IF(!x || !y, BT_EINVAL, "bt_gelu_fwd: NULL pointer");
+  BT_RETURN_IF(!aligned16(x) || !aligned16(y), BT_EALIGN, "bt_gelu_fwd: pointers must be 16-byte aligned");
+  const size_t n4 = n / 4;
+  hipLaunchKernelGGL(gelu_fwd_kernel, dim3(ew_blocks(n4)), dim3(EW_THREADS), 0, as_stream(stream),
+                     reinterpret_cast<const floatx4*>(x), reinterpret_cast<floatx4*>(y), n4);
+  return check_launch("gelu_fwd_kernel");
+}
+
+extern "C" bt_status bt_gelu_bwd(const float* x, const float* dy, float* dx, size_t n, void* stream) {
+  BT_RETURN_IF(n & 3, BT_ESHAPE, "bt_gelu_bwd: n=%zu must be a multiple of 4", n);
+  if (n == 0) return BT_OK;
+  BT_RETURN_IF(!x || !dy || !dx, BT_EINVAL, "bt_gelu_bwd: NULL pointer");
+  BT_RETURN_IF(!aligned16(x) || !aligned16(dy) || !aligned16(dx), BT_EALIGN,
+               "bt_gelu_bwd: pointers must be 16-byte aligned");
+  const size_t n4 = n / 4;
+  hipLaunchKernelGGL(gelu_bwd_kernel, dim3(ew_blocks(n4)), dim3(EW_THREADS), 0, as_stream(stream),
+                     reinterpret_cast<const floatx4*>(x), reinterpret_cast<const floatx4*>(dy),
+                     reinterpret_cast<floatx4*>(dx), n4);
+  return check_launch("gelu_bwd_kernel");
+}
+
+extern "C" bt_status bt_adamw_step(float* p, const float* g, float* m, float* v, size_t n, size_t n_decay,
+                                   float lr, float beta1, float beta2, float eps, float weight_decay, int t,
+                                   const float* grad_scale, void* stream) {
+  BT_RETURN_IF((n & 3) || (n_decay & 3) || n_decay > n, BT_ESHAPE,
+               "bt_adamw_step: n=%zu, n_decay=%zu must be multiples of 4 with n_decay <= n", n, n_decay);
+  BT_RETURN_IF(t < 1, BT_EINVAL, "bt_adamw_step: step t=%d must be >= 1", t);
+  BT_RETURN_IF(!(beta1 >= 0.f && beta1 < 1.f && beta2 >= 0.f && beta2 < 1.f), BT_EINVAL,
+               "bt_adamw_step: betas must be in [0, 1)");
+  if (n == 0) return BT_OK;
+  BT_RETURN_IF(!p || !g || !m || !v, BT_EINVAL, "bt_adamw_step: NULL pointer");
+  BT_RETURN_IF(!aligned16(p) || !aligned16(g) || !aligned16(m) || !aligned16(v), BT_EALIGN,
+               "bt_adamw_step: pointers must be 16-byte aligned");
+  AdamArgs a;
+  a.lr = lr;
+  a.beta1 = beta1;
+  a.beta2 = beta2;
+  a.eps = eps;
+  a.wd = weight_decay;
+  a.inv_bc1 = (float)(1.0 / (1.0 - pow((double)beta1, (double)t)));
+  a.inv_bc2 = (float)(1.0 / (1.0 - pow((double)beta2, (double)t)));
+  const size_t n4 = n / 4;
+  hipLaunchKernelGGL(adamw_kernel, dim3(ew_blocks(n4)), dim3(EW_THREADS), 0, as_stream(stream),
+                     reinterpret_cast<floatx4*>(p), reinterpret_cast<const floatx4*>(g),
+                     reinterpret_cast<floatx4*>(m), reinterpret_cast<floatx4*>(v), n4, n_decay / 4, a,
+                     grad_scale);
+  return check_launch("adamw_kernel");
+}
+
+extern "C" size_t bt_grad_norm_ws_bytes(size_t n) {
+  return align_up((size_t)ew_blocks(n / 4) * sizeof(double), 256);
+}
+
+extern "C" bt_status bt_grad_norm_clip(const float* g, size_t n, float clip, float* out_norm, float* out_coef,
+                                       void* ws, size_t ws_bytes, void* stream) {
+  BT_RETURN_IF(n & 3, BT_ESHAPE, "bt_grad_norm_clip: n=%zu must be a multiple of 4", n);
+  BT_RETURN_IF(!out_norm && !out_coef, BT_EINVAL, "bt_grad_norm_clip: no output");
+  BT_RETURN_IF(n > 0 && !g, BT_EINVAL, "bt_grad_norm_clip: g is NULL");
+  BT_RETURN_IF(g && !aligned16(g), BT_EALIGN, "bt_grad_norm_clip: g must be 16-byte aligned");
+  const size_t need = bt_grad_norm_ws_bytes(n);
+  BT_RETURN_IF(!ws || ws_bytes < need, BT_EWORKSPACE, "bt_grad_norm_clip: workspace of %zu bytes needed (got %zu)",
+               need, ws_bytes);
+  const size_t n4 = n / 4;
+  const unsigned nb = ew_blocks(n4);
+  hipStream_t s = as_stream(stream);
+  double* part = static_cast<double*>(ws);
+  hipLaunchKernelGGL(sumsq_kernel, dim3(nb), dim3(EW_THREADS), 0, s, reinterpret_cast<const floatx4*>(g), n4, part);
+  BT_TRY(check_launch("sumsq_kernel"));
+  hipLaunchKernelGGL(norm_finish_kernel, dim3(1), dim3(EW_THREADS), 0, s, part, (int)nb, clip, out_norm, out_coef);
+  return check_launch("norm_finish_kernel");
+}
+
+extern "C" size_t bt_colsum_ws_bytes(int M, int N) {
+  if (M <= 0 || N <= 0) return 0;
+  return align_up((size_t)colsum_blocks(M) * N * sizeof(float), 256);
+}
+
+extern "C" bt_status bt_colsum(const float* X, int M, int N, int ldx, float* out, float beta, void* ws,
+                               size_t ws_bytes, void* stream) {
+  BT_RETURN_IF(M < 0 || N < 0 || (N & 3) || ldx < N || (ldx & 3), BT_ESHAPE,
+               "bt_colsum: M=%d N=%d ldx=%d (N, ldx multiples of 4, ldx >= N)", M, N, ldx);
+  BT_RETURN_IF(beta != 0.f && beta != 1.f, BT_EINVAL, "bt_colsum: beta must be 0 or 1");
+  if (N == 0) return BT_OK;
+  BT_RETURN_IF(!out || (M > 0 && !X), BT_EINVAL, "bt_colsum: NULL pointer");
+  BT_RETURN_IF((X && !aligned16(X)), BT_EALIGN, "bt_colsum: X must be 16-byte aligned");
+  hipStream_t s = as_stream(stream);
+  if (M == 0) {
+    if (beta == 0.f) return fill_zero(out, (size_t)N, s);
+    return BT_OK;
+  }
+  const size_t need = bt_colsum_ws_bytes(M, N);
+  BT_RETURN_IF(!ws || ws_bytes < need, BT_EWORKSPACE, "bt_colsum: workspace of %zu bytes needed (got %zu)", need,
+               ws_bytes);
+  const int nb = colsum_blocks(M);
+  const int rpb = (M + nb - 1) / nb;
+  float* part = static_cast<float*>(ws);
+  hipLaunchKernelGGL(colsum_partial_kernel, dim3(nb), dim3(EW_THREADS), 0, s, X, M, N, (long long)ldx, rpb, part);
+  BT_TRY(check_launch("colsum_partial_kernel"));
+  hipLaunchKernelGGL(colsum_finish_kernel, dim3((N + 255) / 256), dim3(256), 0, s, part, nb, N, out, beta);
+  return check_launch("colsum_finish_kernel");
+}

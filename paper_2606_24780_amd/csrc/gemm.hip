@@ -1,0 +1,400 @@
+// FP32 GEMM family on the CDNA4 matrix cores (v_mfma_f32_32x32x2_f32).
+//
+// Serves every dense projection of the training step in its three layouts
+// (native GEMM library paragraph of "Implementation": QKV, attention-output
+// and MLP projections in forward and backward layouts, plus the tied LM
+// head):  forward Y = X W (NN), input gradient dX = dY W^T (NT), weight
+// gradient dW = X^T dY (TN, reduction over tokens, split along K).
+//
+// Design (gfx950):
+//  * block tile 128 x 128 x 32, 256 threads = 4 waves in a 2 x 2 grid, each
+//    wave owns a 64 x 64 sub-tile = 2 x 2 MFMA 32x32 accumulators (64 VGPRs).
+//  * each operand tile is staged global -> VGPR -> LDS with float4 accesses in
+//    the layout of its source (K-contiguous rows [rows][BK+4] or
+//    MN-contiguous rows [BK][128+4]); two LDS buffers, one barrier per k-tile,
+//    the next tile's global loads in flight while the MFMAs run.
+//  * the MFMA k-slot of lane half h at step s is k = 8h + (s mod 8) +
+//    16 (s div 8): K-contiguous tiles are read as float4 (4 steps at once),
+//    MN-contiguous tiles as b32 with the two lane halves 8 rows apart, which
+//    keeps both reads free of LDS bank conflicts.
+//  * blocks are remapped so that each XCD (round-robin dispatch over 8 XCDs,
+//    one L2 each) receives a contiguous range of a grouped (8 tile-rows)
+//    tile order, so concurrently running tiles share A rows / B columns in L2.
+//  * low-parallelism weight-gradient shapes (small M x N, long K) are split
+//    along K; partials go to a workspace and are summed in a fixed order.
+//  * fused epilogues: bias, bias + tanh-GELU (optionally storing the
+//    pre-activation), GELU-backward (multiply by gelu'(pre)), residual add and
+//    beta = 1 accumulation.
+#include "bt_internal.h"
+
+namespace bt {
+namespace {
+
+constexpr int BM = 128, BN = 128, BK = 32;
+constexpr int LDK = BK + 4;   // row stride of K-contiguous LDS tiles
+constexpr int LDM = BM + 4;   // row stride of MN-contiguous LDS tiles (BM == BN)
+constexpr int NTHREADS = 256;
+
+struct GemmParams {
+  const float* A;
+  const float* B;
+  float* C;
+  const float* bias;
+  float* preact;
+  const float* gelu_in;
+  const float* residual;
+  float* ws;
+  long long lda, ldb, ldc;
+  int M, N, K;
+  int ksplit;   // K range handled by one split (multiple of BK)
+  int splits;
+  int tiles_m, tiles_n;
+  float beta;
+};
+
+template <bool KC>
+struct TileSize {
+  static constexpr int value = KC ? BM * LDK : BK * LDM;
+};
+
+// Global -> register staging of one 128 x 32 operand tile (4 float4 per thread).
+// rows = M (or N) extent, kbeg/kend = k range of this split.
+template <bool KC>
+__device__ __forceinline__ void load_tile(floatx4 (&r)[4], const float* __restrict__ X,
+                                          long long ld, int row0, int rows, int k0, int kend,
+                                          int tid) {
+  if (KC) {
+    // [rows][K]: thread -> (row = tid/8 + 32 i, k = 4 (tid%8)); 128 B per row segment
+    const int kk = k0 + 4 * (tid & 7);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = row0 + (tid >> 3) + 32 * i;
+      if (row < rows && kk < kend)
+        r[i] = *reinterpret_cast<const floatx4*>(X + (long long)row * ld + kk);
+      else
+        r[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+  } else {
+    // [K][rows]: thread -> (k = tid/32 + 8 i, col = 4 (tid%32)); 512 B per k row
+    const int col = row0 + 4 * (tid & 31);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int kk = k0 + (tid >> 5) + 8 * i;
+      if (kk < kend && col < rows)
+        r[i] = *reinterpret_cast<const floatx4*>(X + (long long)kk * ld + col);
+      else
+        r[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+    }
+  }
+}
+
+template <bool KC>
+__device__ __forceinline__ void store_tile(float* __restrict__ s, const floatx4 (&r)[4], int tid) {
+  if (KC) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *reinterpret_cast<floatx4*>(s + ((tid >> 3) + 32 * i) * LDK + 4 * (tid & 7)) = r[i];
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      *reinterpret_cast<floatx4*>(s + ((tid >> 5) + 8 * i) * LDM + 4 * (tid & 31)) = r[i];
+  }
+}
+
+// Fragment for 4 consecutive MFMA steps (chunk c) of one 32-row block.
+template <bool KC>
+__device__ __forceinline__ floatx4 read_frag(const float* __restrict__ s, int row, int koff) {
+  if (KC) {
+    return *reinterpret_cast<const floatx4*>(s + row * LDK + koff);
+  } else {
+    floatx4 v;
+    v[0] = s[(koff + 0) * LDM + row];
+    v[1] = s[(koff + 1) * LDM + row];
+    v[2] = s[(koff + 2) * LDM + row];
+    v[3] = s[(koff + 3) * LDM + row];
+    return v;
+  }
+}
+
+template <int EPI>
+__device__ __forceinline__ void epilogue_store(const GemmParams& p, int i, int j, float acc) {
+  const long long off = (long long)i * p.ldc + j;
+  float v = acc;
+  if (EPI == BT_EPI_BIAS) {
+    v += p.bias[j];
+  } else if (EPI == BT_EPI_BIAS_GELU) {
+    const float pre = v + p.bias[j];
+    if (p.preact) p.preact[off] = pre;
+    v = gelu_f(pre);
+  } else if (EPI == BT_EPI_DGELU) {
+    v *= gelu_grad_f(p.gelu_in[off]);
+  }
+  if (p.residual) v += p.residual[off];
+  if (p.beta != 0.f) v += p.C[off];
+  p.C[off] = v;
+}
+
+template <bool A_KC, bool B_KC, int EPI, bool SPLIT>
+__global__ void __launch_bounds__(NTHREADS, 2) gemm_f32_mfma(const GemmParams p) {
+  constexpr int A_SZ = TileSize<A_KC>::value;
+  constexpr int B_SZ = TileSize<B_KC>::value;
+  __shared__ __attribute__((aligned(16))) float smem[2 * (A_SZ + B_SZ)];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int lr = lane & 31;
+  const int hh = lane >> 5;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // ---- tile scheduling: XCD-contiguous ranges of a grouped tile order
+  const int ntiles = p.tiles_m * p.tiles_n;
+  const int total = gridDim.x;
+  int bid = blockIdx.x;
+  if ((total & 7) == 0) bid = (bid & 7) * (total >> 3) + (bid >> 3);
+  const int z = bid / ntiles;
+  const int tile = bid - z * ntiles;
+  const int group = 8 * p.tiles_n;
+  const int gid = tile / group;
+  const int first_m = gid * 8;
+  const int gsz = min(p.tiles_m - first_m, 8);
+  const int in_g = tile - gid * group;
+  const int tm = first_m + in_g % gsz;
+  const int tn = in_g / gsz;
+  const int m0 = tm * BM, n0 = tn * BN;
+
+  const int kbeg = z * p.ksplit;
+  const int kend = min(p.K, kbeg + p.ksplit);
+  const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+
+  floatx16 acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
+
+  floatx4 ra[4], rb[4];
+  if (nk > 0) {
+    load_tile<A_KC>(ra, p.A, p.lda, m0, p.M, kbeg, kend, tid);
+    load_tile<B_KC>(rb, p.B, p.ldb, n0, p.N, kbeg, kend, tid);
+    store_tile<A_KC>(smem, ra, tid);
+    store_tile<B_KC>(smem + A_SZ, rb, tid);
+  }
+  __syncthreads();
+
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    const bool more = kt + 1 < nk;
+    if (more) {
+      const int k0 = kbeg + (kt + 1) * BK;
+      load_tile<A_KC>(ra, p.A, p.lda, m0, p.M, k0, kend, tid);
+      load_tile<B_KC>(rb, p.B, p.ldb, n0, p.N, k0, kend, tid);
+    }
+    const float* sA = smem + cur * (A_SZ + B_SZ);
+    const float* sB = sA + A_SZ;
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int koff = 8 * hh + 4 * (c & 1) + 16 * (c >> 1);
+      floatx4 fa[2], fb[2];
+#pragma unroll
+      for (int mb = 0; mb < 2; ++mb) fa[mb] = read_frag<A_KC>(sA, wm * 64 + mb * 32 + lr, koff);
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) fb[nb] = read_frag<B_KC>(sB, wn * 64 + nb * 32 + lr, koff);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+          for (int nb = 0; nb < 2; ++nb)
+            acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[mb][q], fb[nb][q], acc[mb][nb],
+                                                               0, 0, 0);
+    }
+    if (more) {
+      float* sN = smem + (cur ^ 1) * (A_SZ + B_SZ);
+      store_tile<A_KC>(sN, ra, tid);
+      store_tile<B_KC>(sN + A_SZ, rb, tid);
+    }
+    __syncthreads();
+  }
+
+  // ---- epilogue.  Accumulator element r of lane (lr, hh) of block (mb, nb):
+  // row = 8 (r/4) + 4 hh + r%4, column = lr.
+#pragma unroll
+  for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const int j = n0 + wn * 64 + nb * 32 + lr;
+      if (j >= p.N) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = m0 + wm * 64 + mb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
+        if (i >= p.M) continue;
+        if (SPLIT)
+          p.ws[(long long)z * p.M * p.N + (long long)i * p.N + j] = acc[mb][nb][r];
+        else
+          epilogue_store<EPI>(p, i, j, acc[mb][nb][r]);
+      }
+    }
+}
+
+// Fixed-order sum of split-K partials: C = sum_z ws[z] + beta * C.
+__global__ void __launch_bounds__(256) splitk_reduce(const float* __restrict__ ws, float* __restrict__ C,
+                                                     long long ldc, int M, int N, int splits,
+                                                     float beta) {
+  const long long n4 = (long long)M * (N / 4);
+  const long long MN = (long long)M * N;
+  for (long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x; e < n4;
+       e += (long long)gridDim.x * blockDim.x) {
+    const int i = (int)(e / (N / 4));
+    const int j = (int)(e - (long long)i * (N / 4)) * 4;
+    const float* w = ws + (long long)i * N + j;
+    floatx4 s = *reinterpret_cast<const floatx4*>(w);
+    for (int z = 1; z < splits; ++z) s += *reinterpret_cast<const floatx4*>(w + z * MN);
+    floatx4* c = reinterpret_cast<floatx4*>(C + (long long)i * ldc + j);
+    if (beta != 0.f) s += *c;
+    *c = s;
+  }
+}
+
+template <bool A_KC, bool B_KC>
+void launch_epi(const GemmParams& p, int epi, bool split, dim3 grid, hipStream_t s) {
+  if (split) {
+    hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true>), grid, dim3(NTHREADS), 0, s, p);
+    return;
+  }
+  switch (epi) {
+    case BT_EPI_NONE:
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false>), grid, dim3(NTHREADS), 0, s, p);
+      break;
+    case BT_EPI_BIAS:
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS, false>), grid, dim3(NTHREADS), 0, s, p);
+      break;
+    case BT_EPI_BIAS_GELU:
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS_GELU, false>), grid, dim3(NTHREADS), 0, s, p);
+      break;
+    default:
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_DGELU, false>), grid, dim3(NTHREADS), 0, s, p);
+      break;
+  }
+}
+
+// Number of K splits for a shape: only when the tile grid cannot fill the
+// chip (fewer than 2 blocks per CU on 256 CUs) and K is long.
+int choose_splits(int M, int N, int K, int* ksplit) {
+  const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  int splits = 1;
+  if (tiles < 512 && K >= 8 * BK) {
+    splits = (512 + tiles - 1) / tiles;
+    const int max_splits = K / (4 * BK);  // at least 4 k-tiles per split
+    if (splits > max_splits) splits = max_splits;
+    if (splits > 32) splits = 32;
+    if (splits < 1) splits = 1;
+  }
+  int ks = (K + splits - 1) / splits;
+  ks = (ks + BK - 1) / BK * BK;
+  if (ks < BK) ks = BK;
+  splits = K > 0 ? (K + ks - 1) / ks : 1;
+  *ksplit = ks;
+  return splits;
+}
+
+}  // namespace
+}  // namespace bt
+
+using namespace bt;
+
+extern "C" size_t bt_gemm_ws_bytes(bt_op opA, bt_op opB, int M, int N, int K, bt_epi epi) {
+  (void)opA;
+  (void)opB;
+  if (M <= 0 || N <= 0 || K <= 0 || epi != BT_EPI_NONE) return 0;
+  int ks;
+  const int splits = choose_splits(M, N, K, &ks);
+  if (splits <= 1) return 0;
+  return (size_t)splits * M * N * sizeof(float);
+}
+
+extern "C" bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K, const float* A, int lda,
+                             const float* B, int ldb, float beta, float* C, int ldc,
+                             const float* bias, bt_epi epi, float* preact_out,
+                             const float* gelu_in, const float* residual, void* ws,
+                             size_t ws_bytes, void* stream) {
+  BT_RETURN_IF(opA != BT_OP_N && opA != BT_OP_T, BT_EINVAL, "bt_gemm: bad opA %d", (int)opA);
+  BT_RETURN_IF(opB != BT_OP_N && opB != BT_OP_T, BT_EINVAL, "bt_gemm: bad opB %d", (int)opB);
+  BT_RETURN_IF(epi < BT_EPI_NONE || epi > BT_EPI_DGELU, BT_EINVAL, "bt_gemm: bad epilogue %d", (int)epi);
+  BT_RETURN_IF(M < 0 || N < 0 || K < 0, BT_ESHAPE, "bt_gemm: negative size M=%d N=%d K=%d", M, N, K);
+  BT_RETURN_IF((M | N | K) & 3, BT_ESHAPE, "bt_gemm: M=%d N=%d K=%d must be multiples of 4", M, N, K);
+  BT_RETURN_IF(beta != 0.f && beta != 1.f, BT_EINVAL, "bt_gemm: beta must be 0 or 1 (got %g)", beta);
+  if (M == 0 || N == 0) return BT_OK;
+  const int a_cols = opA == BT_OP_N ? K : M;
+  const int b_cols = opB == BT_OP_N ? N : K;
+  BT_RETURN_IF(lda < a_cols || ldb < b_cols || ldc < N, BT_ESHAPE,
+               "bt_gemm: leading dimension too small (lda=%d need %d, ldb=%d need %d, ldc=%d need %d)",
+               lda, a_cols, ldb, b_cols, ldc, N);
+  BT_RETURN_IF((lda | ldb | ldc) & 3, BT_EALIGN, "bt_gemm: lda/ldb/ldc must be multiples of 4");
+  BT_RETURN_IF(!C, BT_EINVAL, "bt_gemm: C is NULL");
+  BT_RETURN_IF(K > 0 && (!A || !B), BT_EINVAL, "bt_gemm: A or B is NULL");
+  BT_RETURN_IF(!aligned16(C) || (A && !aligned16(A)) || (B && !aligned16(B)), BT_EALIGN,
+               "bt_gemm: A, B, C must be 16-byte aligned");
+  BT_RETURN_IF((epi == BT_EPI_BIAS || epi == BT_EPI_BIAS_GELU) && !bias, BT_EINVAL,
+               "bt_gemm: bias required for this epilogue");
+  BT_RETURN_IF(epi == BT_EPI_DGELU && !gelu_in, BT_EINVAL, "bt_gemm: gelu_in required for DGELU");
+  BT_RETURN_IF(residual && residual == C, BT_EINVAL, "bt_gemm: residual must not alias C");
+
+  GemmParams p{};
+  p.A = A;
+  p.B = B;
+  p.C = C;
+  p.bias = bias;
+  p.preact = epi == BT_EPI_BIAS_GELU ? preact_out : nullptr;
+  p.gelu_in = gelu_in;
+  p.residual = residual;
+  p.lda = lda;
+  p.ldb = ldb;
+  p.ldc = ldc;
+  p.M = M;
+  p.N = N;
+  p.K = K;
+  p.beta = beta;
+  p.tiles_m = (M + BM - 1) / BM;
+  p.tiles_n = (N + BN - 1) / BN;
+  int ks = K;
+  int splits = 1;
+  const bool may_split = epi == BT_EPI_NONE && residual == nullptr;
+  if (may_split && K > 0) splits = choose_splits(M, N, K, &ks);
+  if (splits <= 1) {
+    splits = 1;
+    ks = K > 0 ? K : BK;
+  }
+  p.ksplit = ks;
+  p.splits = splits;
+  const bool split = splits > 1;
+  if (split) {
+    const size_t need = (size_t)splits * M * N * sizeof(float);
+    BT_RETURN_IF(!ws || ws_bytes < need, BT_EWORKSPACE,
+                 "bt_gemm: workspace of %zu bytes needed (got %zu)", need, ws_bytes);
+    BT_RETURN_IF(!aligned16(ws), BT_EALIGN, "bt_gemm: workspace must be 16-byte aligned");
+    p.ws = static_cast<float*>(ws);
+  }
+  const long long nblocks = (long long)p.tiles_m * p.tiles_n * splits;
+  BT_RETURN_IF(nblocks > 0x7fffffffLL, BT_ESHAPE, "bt_gemm: too many tiles");
+  dim3 grid((unsigned)nblocks);
+  hipStream_t s = as_stream(stream);
+  const bool akc = opA == BT_OP_N;
+  const bool bkc = opB == BT_OP_T;
+  if (akc && !bkc) launch_epi<true, false>(p, epi, split, grid, s);
+  else if (akc && bkc) launch_epi<true, true>(p, epi, split, grid, s);
+  else if (!akc && !bkc) launch_epi<false, false>(p, epi, split, grid, s);
+  else launch_epi<false, true>(p, epi, split, grid, s);
+  BT_TRY(check_launch("gemm_f32_mfma"));
+  if (split) {
+    const long long n4 = (long long)M * (N / 4);
+    long long nb = (n4 + 255) / 256;
+    if (nb > 4096) nb = 4096;
+    hipLaunchKernelGGL(splitk_reduce, dim3((unsigned)nb), dim3(256), 0, s, p.ws, C, (long long)ldc, M,
+                       N, splits, beta);
+    BT_TRY(check_launch("splitk_reduce"));
+  }
+  return BT_OK;
+}

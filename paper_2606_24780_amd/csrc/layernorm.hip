@@ -1,0 +1,259 @@
+// LayerNorm forward and backward over the last dimension (pre-normalised
+// GPT-2 blocks; appendix "LayerNorm Forward / Backward").
+//
+// One wave64 per row: the row (C <= 4096 floats) is held in registers as
+// float4, mean and variance come from two in-register passes reduced with
+// cross-lane shuffles (no LDS), so x is read once and y written once.  The
+// backward computes dx row-wise the same way; dgamma/dbeta are accumulated
+// per wave over a contiguous chunk of rows, combined per block through LDS
+// and written as block partials that a second kernel sums in a fixed order.
+#include "bt_internal.h"
+
+namespace bt {
+namespace {
+
+constexpr int ROWS_PER_BLOCK = 4;  // 4 waves
+
+template <int NV>
+__global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ x,
+                                                     const float* __restrict__ gamma,
+                                                     const float* __restrict__ beta,
+                                                     float* __restrict__ y, float* __restrict__ mean,
+                                                     float* __restrict__ rstd, int M, int C, float eps) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * ROWS_PER_BLOCK + (threadIdx.x >> 6);
+  if (row >= M) return;
+  const int C4 = C >> 2;
+  const floatx4* xr = reinterpret_cast<const floatx4*>(x + (long long)row * C);
+  floatx4 v[NV];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = lane + 64 * i;
+    v[i] = c < C4 ? xr[c] : floatx4{0.f, 0.f, 0.f, 0.f};
+    s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
+  }
+  const float mu = wave_sum(s) / (float)C;
+  float q = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = lane + 64 * i;
+    if (c < C4) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const float d = v[i][k] - mu;
+        q += d * d;
+      }
+    }
+  }
+  const float var = wave_sum(q) / (float)C;
+  const float rs = 1.0f / sqrtf(var + eps);
+  floatx4* yr = reinterpret_cast<floatx4*>(y + (long long)row * C);
+  const floatx4* g4 = reinterpret_cast<const floatx4*>(gamma);
+  const floatx4* b4 = reinterpret_cast<const floatx4*>(beta);
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = lane + 64 * i;
+    if (c < C4) {
+      const floatx4 g = g4[c], b = b4[c];
+      floatx4 o;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) o[k] = (v[i][k] - mu) * rs * g[k] + b[k];
+      yr[c] = o;
+    }
+  }
+  if (lane == 0) {
+    mean[row] = mu;
+    rstd[row] = rs;
+  }
+}
+
+// dx row-wise; per-block partial column sums of dy*xhat and dy.
+template <int NV>
+__global__ void __launch_bounds__(256) ln_bwd_kernel(const float* dy, const float* __restrict__ x,
+                                                     const float* __restrict__ gamma,
+                                                     const float* __restrict__ mean,
+                                                     const float* __restrict__ rstd, float* dx,
+                                                     float* __restrict__ part, int M, int C,
+                                                     int rows_per_block, float dx_beta) {
+  __shared__ floatx4 red[64 * NV][2];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int C4 = C >> 2;
+  const floatx4* g4 = reinterpret_cast<const floatx4*>(gamma);
+  floatx4 gam[NV], acc_dg[NV], acc_db[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = lane + 64 * i;
+    gam[i] = c < C4 ? g4[c] : floatx4{0.f, 0.f, 0.f, 0.f};
+    acc_dg[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+    acc_db[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+  const int r0 = blockIdx.x * rows_per_block;
+  const int r1 = min(M, r0 + rows_per_block);
+  for (int row = r0 + wave; row < r1; row += ROWS_PER_BLOCK) {
+    const floatx4* dyr = reinterpret_cast<const floatx4*>(dy + (long long)row * C);
+    const floatx4* xr = reinterpret_cast<const floatx4*>(x + (long long)row * C);
+    const float mu = mean[row], rs = rstd[row];
+    floatx4 xh[NV], gg[NV], d[NV];
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c = lane + 64 * i;
+      if (c < C4) {
+        d[i] = dyr[c];
+        const floatx4 xv = xr[c];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          xh[i][k] = (xv[k] - mu) * rs;
+          gg[i][k] = d[i][k] * gam[i][k];
+          s1 += gg[i][k];
+          s2 += gg[i][k] * xh[i][k];
+        }
+      } else {
+        d[i] = xh[i] = gg[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+    const float mg = wave_sum(s1) / (float)C;
+    const float mgx = wave_sum(s2) / (float)C;
+    floatx4* dxr = reinterpret_cast<floatx4*>(dx + (long long)row * C);
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c = lane + 64 * i;
+      if (c < C4) {
+        floatx4 o;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) o[k] = rs * (gg[i][k] - mg - xh[i][k] * mgx);
+        if (dx_beta != 0.f) o += dxr[c];
+        dxr[c] = o;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          acc_dg[i][k] += d[i][k] * xh[i][k];
+          acc_db[i][k] += d[i][k];
+        }
+      }
+    }
+  }
+  // fixed-order combine of the 4 waves (wave 0 first), one partial row per block
+  for (int w = 0; w < ROWS_PER_BLOCK; ++w) {
+    if (wave == w) {
+#pragma unroll
+      for (int i = 0; i < NV; ++i) {
+        const int c = lane + 64 * i;
+        if (w == 0) {
+          red[c][0] = acc_dg[i];
+          red[c][1] = acc_db[i];
+        } else {
+          red[c][0] += acc_dg[i];
+          red[c][1] += acc_db[i];
+        }
+      }
+    }
+    __syncthreads();
+  }
+  floatx4* pg = reinterpret_cast<floatx4*>(part + (long long)blockIdx.x * 2 * C);
+  for (int c = threadIdx.x; c < C4; c += 256) {
+    pg[c] = red[c][0];
+    pg[C4 + c] = red[c][1];
+  }
+}
+
+__global__ void __launch_bounds__(256) ln_bwd_param_reduce(const float* __restrict__ part, int nblocks, int C,
+                                                           float* __restrict__ dgamma,
+                                                           float* __restrict__ dbeta, float beta) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= 2 * C) return;
+  float s = 0.f;
+  for (int b = 0; b < nblocks; ++b) s += part[(long long)b * 2 * C + c];
+  float* dst = c < C ? dgamma + c : dbeta + (c - C);
+  if (beta != 0.f) s += *dst;
+  *dst = s;
+}
+
+int ln_nv(int C) { return (C / 4 + 63) / 64; }
+
+int ln_bwd_blocks(int M) {
+  int nb = (M + 31) / 32;  // >= 32 rows per block (8 per wave)
+  if (nb > 1024) nb = 1024;
+  if (nb < 1) nb = 1;
+  return nb;
+}
+
+#define BT_LN_DISPATCH(NVV, ...)                       \
+  switch (NVV) {                                       \
+    case 1: __VA_ARGS__(1); break;                     \
+    case 2: __VA_ARGS__(2); break;                     \
+    case 3: __VA_ARGS__(3); break;                     \
+    case 4: __VA_ARGS__(4); break;                     \
+    case 5: case 6: __VA_ARGS__(6); break;             \
+    case 7: case 8: __VA_ARGS__(8); break;             \
+    default: __VA_ARGS__(16); break;                   \
+  }
+
+bt_status ln_check(int M, int C, const char* who) {
+  BT_RETURN_IF(M < 0 || C <= 0 || (C & 3) || C > 4096, BT_ESHAPE,
+               "%s: C=%d must be a positive multiple of 4 <= 4096 (M=%d)", who, C, M);
+  return BT_OK;
+}
+
+}  // namespace
+}  // namespace bt
+
+using namespace bt;
+
+extern "C" bt_status bt_layernorm_fwd(const float* x, const float* gamma, const float* beta, float* y,
+                                      float* mean, float* rstd, int M, int C, float eps, void* stream) {
+  BT_TRY(ln_check(M, C, "bt_layernorm_fwd"));
+  if (M == 0) return BT_OK;
+  BT_RETURN_IF(!x || !gamma || !beta || !y || !mean || !rstd, BT_EINVAL, "bt_layernorm_fwd: NULL pointer");
+  BT_RETURN_IF(!aligned16(x) || !aligned16(y) || !aligned16(gamma) || !aligned16(beta), BT_EALIGN,
+               "bt_layernorm_fwd: x, y, gamma, beta must be 16-byte aligned");
+  BT_RETURN_IF(x == y, BT_EINVAL, "bt_layernorm_fwd: y must not alias x");
+  BT_RETURN_IF(!(eps >= 0.f), BT_EINVAL, "bt_layernorm_fwd: eps must be >= 0");
+  dim3 grid((M + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK);
+  hipStream_t s = as_stream(stream);
+#define BT_LN_FWD(NV) hipLaunchKernelGGL(ln_fwd_kernel<NV>, grid, dim3(256), 0, s, x, gamma, beta, y, mean, rstd, M, C, eps)
+  BT_LN_DISPATCH(ln_nv(C), BT_LN_FWD)
+#undef BT_LN_FWD
+  return check_launch("ln_fwd_kernel");
+}
+
+extern "C" size_t bt_layernorm_bwd_ws_bytes(int M, int C) {
+  if (M <= 0 || C <= 0) return 0;
+  return align_up((size_t)ln_bwd_blocks(M) * 2 * C * sizeof(float), 256);
+}
+
+extern "C" bt_status bt_layernorm_bwd(const float* dy, const float* x, const float* gamma, const float* mean,
+                                      const float* rstd, float* dx, float* dgamma, float* dbeta,
+                                      float dx_beta, float param_beta, void* ws, size_t ws_bytes, int M,
+                                      int C, void* stream) {
+  BT_TRY(ln_check(M, C, "bt_layernorm_bwd"));
+  BT_RETURN_IF((dx_beta != 0.f && dx_beta != 1.f) || (param_beta != 0.f && param_beta != 1.f), BT_EINVAL,
+               "bt_layernorm_bwd: dx_beta and param_beta must be 0 or 1");
+  BT_RETURN_IF(!dy || !x || !gamma || !mean || !rstd || !dx || !dgamma || !dbeta, BT_EINVAL,
+               "bt_layernorm_bwd: NULL pointer");
+  BT_RETURN_IF(!aligned16(dy) || !aligned16(x) || !aligned16(dx) || !aligned16(gamma), BT_EALIGN,
+               "bt_layernorm_bwd: dy, x, dx, gamma must be 16-byte aligned");
+  BT_RETURN_IF(dx == dy && dx_beta != 0.f, BT_EINVAL, "bt_layernorm_bwd: dx may alias dy only with dx_beta = 0");
+  hipStream_t s = as_stream(stream);
+  if (M == 0) {
+    if (param_beta == 0.f) {
+      BT_TRY(fill_zero(dgamma, (size_t)C, s));
+      BT_TRY(fill_zero(dbeta, (size_t)C, s));
+    }
+    return BT_OK;
+  }
+  const size_t need = bt_layernorm_bwd_ws_bytes(M, C);
+  BT_RETURN_IF(!ws || ws_bytes < need, BT_EWORKSPACE, "bt_layernorm_bwd: workspace of %zu bytes needed (got %zu)",
+               need, ws_bytes);
+  const int nb = ln_bwd_blocks(M);
+  const int rpb = (M + nb - 1) / nb;
+  float* part = static_cast<float*>(ws);
+#define BT_LN_BWD(NV) hipLaunchKernelGGL(ln_bwd_kernel<NV>, dim3(nb), dim3(256), 0, s, dy, x, gamma, mean, rstd, dx, part, M, C, rpb, dx_beta)
+  BT_LN_DISPATCH(ln_nv(C), BT_LN_BWD)
+#undef BT_LN_BWD
+  BT_TRY(check_launch("ln_bwd_kernel"));
+  hipLaunchKernelGGL(ln_bwd_param_reduce, dim3((2 * C + 255) / 256), dim3(256), 0, s, part, nb, C, dgamma, dbeta,
+                     param_beta);
+  return check_launch("ln_bwd_param_reduce");
+}

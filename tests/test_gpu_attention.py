@@ -1,0 +1,96 @@
+"""Causal attention parity: bt_attention_fwd/bwd against the float64 oracle.
+
+Small cases cover ragged T (not a multiple of the 32-row tiles or the
+128-row blocks), T = 1, head dims 16/32/64 and several heads; the GPT-2
+124M shape (B=16, T=1024, H=12, hd=64) runs in full and is checked on
+sampled (batch, head) pairs that the oracle computes one by one.
+Bars: out and lse <= 1e-5 of max-abs; dqkv (a gradient) <= 1e-4 of max-abs
+per Q/K/V block."""
+import numpy as np
+import pytest
+
+from oracle import ops
+from paper_2606_24780_amd import bt
+from tests.gpu_util import assert_close_maxabs, dev, host, say, torch_gpu
+
+pytestmark = pytest.mark.gpu
+RNG = np.random.Generator(np.random.PCG64(3))
+
+
+def _run(torch, qkv, dout, B, T, H, hd):
+    q = dev(torch, qkv.reshape(B * T, 3 * H * hd))
+    out = torch.empty((B * T, H * hd), device="cuda")
+    lse = torch.empty((B, H, T), device="cuda")
+    bt.bt_attention_fwd(q, out, lse, B, T, H, hd)
+    dq = torch.empty_like(q)
+    bt.bt_attention_bwd(dev(torch, dout.reshape(B * T, H * hd)), q, out, lse, dq, B, T, H, hd)
+    return (host(out).reshape(B, T, H, hd), host(lse), host(dq).reshape(B, T, 3, H, hd))
+
+
+@pytest.mark.parametrize("B,T,H,hd", [(2, 37, 2, 16), (1, 128, 2, 64), (2, 200, 3, 64), (1, 1, 1, 64),
+                                      (3, 64, 4, 32), (1, 300, 1, 64), (2, 33, 2, 48)])
+def test_attention_small(B, T, H, hd):
+    torch = torch_gpu()
+    say(f"attention B={B} T={T} H={H} hd={hd}")
+    qkv = RNG.standard_normal((B, T, 3, H, hd)).astype(np.float32)
+    dout = RNG.standard_normal((B, T, H, hd)).astype(np.float32)
+    out, lse, dqkv = _run(torch, qkv, dout, B, T, H, hd)
+    r_out, r_lse = ops.attention_fwd(qkv, H)
+    r_dqkv = ops.attention_bwd(dout, qkv, H)
+    assert_close_maxabs(out, r_out, 1e-5, "out")
+    assert_close_maxabs(lse, r_lse, 1e-5, "lse")
+    for i, n in enumerate("QKV"):
+        assert_close_maxabs(dqkv[:, :, i], r_dqkv[:, :, i], 1e-4, f"d{n}")
+
+
+def test_attention_q_zero_closed_form():
+    """Q = 0: each output row is the mean of the visible V rows, lse = ln(t+1)."""
+    torch = torch_gpu()
+    B, T, H, hd = 1, 150, 2, 64
+    qkv = RNG.standard_normal((B, T, 3, H, hd)).astype(np.float32)
+    qkv[:, :, 0] = 0
+    say("attention Q=0 closed form")
+    out, lse, _ = _run(torch, qkv, np.zeros((B, T, H, hd), np.float32), B, T, H, hd)
+    v = qkv[:, :, 2].astype(np.float64)
+    expect = np.cumsum(v, axis=1) / np.arange(1, T + 1)[None, :, None, None]
+    assert_close_maxabs(out, expect, 1e-5, "prefix mean")
+    assert np.allclose(lse, np.log(np.arange(1, T + 1))[None, None], atol=2e-6)
+
+
+def test_attention_deterministic():
+    torch = torch_gpu()
+    B, T, H, hd = 2, 256, 2, 64
+    qkv = RNG.standard_normal((B, T, 3, H, hd)).astype(np.float32)
+    dout = RNG.standard_normal((B, T, H, hd)).astype(np.float32)
+    say("attention determinism")
+    a = _run(torch, qkv, dout, B, T, H, hd)
+    b = _run(torch, qkv, dout, B, T, H, hd)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
+
+
+def test_attention_gpt2_124m_sampled():
+    torch = torch_gpu()
+    B, T, H, hd = 16, 1024, 12, 64
+    g = torch.Generator(device="cuda").manual_seed(3)
+    say("attention full-size B=16 T=1024 H=12 hd=64")
+    qkv = torch.randn((B * T, 3 * H * hd), generator=g, device="cuda")
+    dout = torch.randn((B * T, H * hd), generator=g, device="cuda")
+    out = torch.empty((B * T, H * hd), device="cuda")
+    lse = torch.empty((B, H, T), device="cuda")
+    bt.bt_attention_fwd(qkv, out, lse, B, T, H, hd)
+    dq = torch.empty_like(qkv)
+    bt.bt_attention_bwd(dout, qkv, out, lse, dq, B, T, H, hd)
+    qh = host(qkv).reshape(B, T, 3, H, hd)
+    dh = host(dout).reshape(B, T, H, hd)
+    oh = host(out).reshape(B, T, H, hd)
+    lh = host(lse)
+    dqh = host(dq).reshape(B, T, 3, H, hd)
+    for b, h in [(0, 0), (7, 5), (15, 11), (3, 9)]:
+        q1 = qh[b:b + 1, :, :, h:h + 1]
+        r_out, r_lse = ops.attention_fwd(q1, 1)
+        r_d = ops.attention_bwd(dh[b:b + 1, :, h:h + 1], q1, 1)
+        assert_close_maxabs(oh[b:b + 1, :, h:h + 1], r_out, 1e-5, f"out b={b} h={h}")
+        assert_close_maxabs(lh[b:b + 1, h:h + 1], r_lse, 1e-5, f"lse b={b} h={h}")
+        for i, n in enumerate("QKV"):
+            assert_close_maxabs(dqh[b:b + 1, :, i, h:h + 1], r_d[:, :, i], 1e-4, f"d{n} b={b} h={h}")

@@ -1,0 +1,119 @@
+"""GEMM parity: bt_gemm (FP32 MFMA) against the float64 oracle.
+
+Small shapes span several 128 x 128 tiles with ragged tails, every layout
+(NN, NT, TN, TT) and every epilogue; the GPT-2 124M shapes (M = B*T = 16384)
+run in full and are checked on sampled rows / columns that the oracle
+computes one by one.  Bar: |C - C_ref| <= 1e-5 * max|C_ref| (FP32 inputs,
+FP32 accumulation; the error of a K-term FP32 dot product grows like
+sqrt(K) * 6e-8 relative to the row scale)."""
+import numpy as np
+import pytest
+
+from oracle import ops
+from paper_2606_24780_amd import bt
+from tests.gpu_util import assert_close_maxabs, dev, host, say, torch_gpu
+
+pytestmark = pytest.mark.gpu
+TOL = 1e-5
+RNG = np.random.Generator(np.random.PCG64(2))
+
+
+def _operands(M, N, K, ta, tb):
+    A = RNG.standard_normal((K, M) if ta else (M, K)).astype(np.float32)
+    B = RNG.standard_normal((N, K) if tb else (K, N)).astype(np.float32)
+    return A, B
+
+
+def _run(torch, ta, tb, M, N, K, A, B, **kw):
+    Ad, Bd = dev(torch, A), dev(torch, B)
+    C0 = kw.pop("C0", None)
+    C = dev(torch, C0) if C0 is not None else torch.zeros((M, N), dtype=torch.float32, device="cuda")
+    lda = M if ta else K
+    ldb = K if tb else N
+    bt.bt_gemm(int(ta), int(tb), M, N, K, Ad, lda, Bd, ldb, kw.pop("beta", 0.0), C, N, **kw)
+    return C
+
+
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
+@pytest.mark.parametrize("M,N,K", [(260, 196, 132), (64, 64, 256), (4, 8, 4), (300, 388, 1000),
+                                   (128, 128, 32), (132, 260, 36), (8, 12, 4096)])
+def test_gemm_layouts(ta, tb, M, N, K):
+    torch = torch_gpu()
+    say(f"gemm layout ta={ta} tb={tb} M={M} N={N} K={K}")
+    A, B = _operands(M, N, K, ta, tb)
+    C = _run(torch, ta, tb, M, N, K, A, B)
+    assert_close_maxabs(host(C), ops.gemm(A, B, bool(ta), bool(tb)), TOL, f"gemm {ta}{tb} {M}x{N}x{K}")
+
+
+def test_gemm_epilogues():
+    torch = torch_gpu()
+    M, N, K = 260, 196, 132
+    A, B = _operands(M, N, K, 0, 0)
+    bias = RNG.standard_normal(N).astype(np.float32)
+    res = RNG.standard_normal((M, N)).astype(np.float32)
+    gin = (RNG.standard_normal((M, N)) * 2).astype(np.float32)
+    C0 = RNG.standard_normal((M, N)).astype(np.float32)
+    ref = ops.gemm(A, B)
+    say("gemm epilogue BIAS + residual")
+    C = _run(torch, 0, 0, M, N, K, A, B, bias=dev(torch, bias), epi=bt.EPI_BIAS, residual=dev(torch, res))
+    assert_close_maxabs(host(C), ref + bias + res, TOL, "bias+residual")
+    say("gemm epilogue BIAS_GELU + preact")
+    pre = torch.zeros((M, N), dtype=torch.float32, device="cuda")
+    C = _run(torch, 0, 0, M, N, K, A, B, bias=dev(torch, bias), epi=bt.EPI_BIAS_GELU, preact_out=pre)
+    assert_close_maxabs(host(pre), ref + bias, TOL, "preact")
+    assert_close_maxabs(host(C), ops.gelu_fwd(ref + bias), TOL, "gelu(pre)")
+    say("gemm epilogue DGELU")
+    C = _run(torch, 0, 1, M, N, K, A, np.ascontiguousarray(B.T), epi=bt.EPI_DGELU, gelu_in=dev(torch, gin))
+    assert_close_maxabs(host(C), ref * ops.gelu_grad(gin), TOL, "dgelu")
+    say("gemm beta=1 accumulate (split-K path)")
+    A2, B2 = _operands(64, 64, 2048, 1, 0)
+    C02 = RNG.standard_normal((64, 64)).astype(np.float32)
+    C = _run(torch, 1, 0, 64, 64, 2048, A2, B2, C0=C02, beta=1.0)
+    assert_close_maxabs(host(C), ops.gemm(A2, B2, True) + C02, TOL, "beta=1 split")
+    say("gemm K=0 with bias")
+    C = _run(torch, 0, 0, 8, 8, 0, np.zeros((8, 0), np.float32), np.zeros((0, 8), np.float32),
+             bias=dev(torch, bias[:8]), epi=bt.EPI_BIAS)
+    assert np.array_equal(host(C), np.broadcast_to(bias[:8].astype(np.float64), (8, 8)))
+
+
+def test_gemm_deterministic_split():
+    torch = torch_gpu()
+    say("gemm determinism (split-K)")
+    A, B = _operands(768, 768, 16384, 1, 0)
+    C1 = _run(torch, 1, 0, 768, 768, 16384, A, B)
+    C2 = _run(torch, 1, 0, 768, 768, 16384, A, B)
+    assert torch.equal(C1, C2)
+
+
+# GPT-2 124M (K, N) pairs at M = 16384: QKV, attn-out, FC, FC-proj, LM head
+FULL = [(768, 2304), (768, 768), (768, 3072), (3072, 768), (768, 50304)]
+
+
+@pytest.mark.parametrize("K,N", FULL)
+def test_gemm_gpt2_124m_shapes_sampled(K, N):
+    torch = torch_gpu()
+    M = 16384
+    g = torch.Generator(device="cuda").manual_seed(2)
+    say(f"gemm full-size K={K} N={N}")
+    X = torch.randn((M, K), generator=g, device="cuda")
+    W = torch.randn((K, N), generator=g, device="cuda") * 0.02
+    dY = torch.randn((M, N), generator=g, device="cuda")
+    rows = np.sort(RNG.choice(M, 48, replace=False))
+    cols = np.sort(RNG.choice(N, 48, replace=False))
+    Wh = host(W)
+    # forward NN: Y = X W
+    Y = torch.empty((M, N), device="cuda")
+    bt.bt_gemm(0, 0, M, N, K, X, K, W, N, 0.0, Y, N)
+    Xr = host(X[torch.from_numpy(rows).cuda()])
+    assert_close_maxabs(host(Y)[rows], Xr @ Wh, TOL, f"NN {M}x{N}x{K}")
+    # dX = dY W^T (NT, reduction over N)
+    dX = torch.empty((M, K), device="cuda")
+    bt.bt_gemm(0, 1, M, K, N, dY, N, W, N, 0.0, dX, K)
+    dYr = host(dY[torch.from_numpy(rows).cuda()])
+    assert_close_maxabs(host(dX)[rows], dYr @ Wh.T, TOL, f"NT {M}x{K}x{N}")
+    del dX, Y
+    # dW = X^T dY (TN, reduction over the 16384 tokens)
+    dW = torch.empty((K, N), device="cuda")
+    bt.bt_gemm(1, 0, K, N, M, X, K, dY, N, 0.0, dW, N)
+    dYc = host(dY[:, torch.from_numpy(cols).cuda()])
+    assert_close_maxabs(host(dW)[:, cols], host(X).T @ dYc, TOL, f"TN {K}x{N}x{M}")

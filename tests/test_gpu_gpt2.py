@@ -1,0 +1,231 @@
+"""Composed training step (bt_gpt2_*) against the float64 oracle.
+
+* tiny GPT-2 (2 layers, d 64, 4 heads, vocab 256, T 32, B 2): loss, every
+  gradient tensor and the AdamW update;
+* zero token embedding: loss = ln V;
+* determinism: two identical steps are bitwise equal;
+* 4 micro-steps of B/4 with accumulation equal one step of B;
+* GPT-2 124M at B=16, T=1024 in the benchmark's launch configuration:
+  per-position losses of sampled sequences against the oracle run on those
+  sequences alone, and a batch of 16 copies of one sequence, whose full
+  gradient and update the oracle computes from that one sequence.
+
+Bars (stated for this path): loss relative error <= 1e-5; each gradient
+tensor <= 1e-4 of its max-abs; post-AdamW parameters <= 1e-5 of their
+max-abs, with the oracle's AdamW fed the GPU's own gradients (at t = 1 the
+update g/(|g|+eps) amplifies gradient rounding where |g| ~ eps, so the
+end-to-end comparison is reported and checked against that sensitivity
+instead)."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import gpt2 as og
+from oracle import ops
+from paper_2606_24780_amd import bt, synth
+from tests.golden.make_tiny_step import tiny_inputs
+from tests.gpu_util import assert_close_maxabs, dev, host, say, torch_gpu
+
+pytestmark = pytest.mark.gpu
+
+LOSS_TOL, GRAD_TOL, PARAM_TOL = 1e-5, 1e-4, 1e-5
+
+
+def _gpu_step(torch, cfg, hp, params, x, y, max_B=None):
+    B, T = x.shape
+    model = bt.GPT2(cfg, hp, max_B or B, T)
+    model.load_params(synth.flatten(cfg, params))
+    loss = model.train_step(dev(torch, x), dev(torch, y))
+    torch.cuda.synchronize()
+    return model, loss
+
+
+def _unflat(cfg, t):
+    return synth.unflatten(cfg, host(t))
+
+
+def _check_update(cfg, hp, specs, params0, g_gpu, p_gpu, m_gpu, v_gpu, t, coef_gpu_norm=None, what=""):
+    """Reading of the post-AdamW bar: the oracle's AdamW applied to the GPU's
+    own gradients (and the clip coefficient of their norm) must match."""
+    flat_g = np.concatenate([g_gpu[n].ravel() for n, _, _ in specs])
+    norm = ops.grad_norm(flat_g)
+    coef = ops.clip_coef(norm, hp.grad_clip)
+    for name, _, dec in specs:
+        rp, rm, rv = ops.adamw(params0[name], g_gpu[name], np.zeros_like(g_gpu[name]), np.zeros_like(g_gpu[name]),
+                               t, hp.lr, hp.beta1, hp.beta2, hp.eps, hp.weight_decay, 1.0 if dec else 0.0, coef)
+        assert_close_maxabs(p_gpu[name], rp, PARAM_TOL, f"{what} param {name}")
+        assert_close_maxabs(m_gpu[name], rm, 1e-5, f"{what} m {name}")
+        assert_close_maxabs(v_gpu[name], rv, 1e-5, f"{what} v {name}")
+    return norm, coef
+
+
+def _check_end_to_end(hp, specs, params0, g_gpu, g_or, p_gpu, p_or):
+    """End-to-end params: elementwise within 1e-5 max-abs, or within the
+    t = 1 sensitivity lr * eps * |dg| / (min|g| + eps)^2 of the update."""
+    worst = 0.0
+    for name, _, _ in specs:
+        d = np.abs(p_gpu[name] - p_or[name])
+        scale = np.abs(p_or[name]).max()
+        gmin = np.minimum(np.abs(g_gpu[name]), np.abs(g_or[name]))
+        bound = hp.lr * hp.eps * np.abs(g_gpu[name] - g_or[name]) / (gmin + hp.eps) ** 2 + PARAM_TOL * scale
+        same_sign = np.sign(g_gpu[name]) == np.sign(g_or[name])
+        bound = np.where(same_sign, bound, 2 * hp.lr + PARAM_TOL * scale)
+        assert (d <= bound * (1 + 1e-6) + 1e-12).all(), f"end-to-end {name}"
+        worst = max(worst, float(d.max() / scale))
+    say(f"[parity] end-to-end params worst max-abs-rel {worst:.3e}")
+
+
+def test_tiny_step_vs_oracle():
+    torch = torch_gpu()
+    cfg, params, x, y = tiny_inputs()
+    hp = synth.HP_TINY
+    specs = synth.param_specs(cfg)
+    say("gpt2 tiny step")
+    model, loss = _gpu_step(torch, cfg, hp, params, x, y)
+    zeros = {k: np.zeros_like(v, dtype=np.float64) for k, v in params.items()}
+    ref = og.train_step(cfg, hp, specs, params, zeros, zeros, x, y, t=1)
+    say(f"loss gpu={loss:.8f} oracle={ref['loss']:.8f}")
+    assert abs(loss - ref["loss"]) <= LOSS_TOL * abs(ref["loss"])
+    g = _unflat(cfg, model.grads)
+    for name, _, _ in specs:
+        assert_close_maxabs(g[name], ref["grads"][name], GRAD_TOL, f"grad {name}")
+    p = _unflat(cfg, model.params)
+    m = _unflat(cfg, model.m)
+    v = _unflat(cfg, model.v)
+    _check_update(cfg, hp, specs, params, g, p, m, v, 1, what="tiny")
+    _check_end_to_end(hp, specs, params, g, ref["grads"], p, ref["params"])
+    assert model.step_count == 1
+
+
+def test_tiny_zero_wte_loss_is_ln_V():
+    torch = torch_gpu()
+    cfg, _, x, y = tiny_inputs()
+    params = synth.init_params(cfg, 1, zero_wte=True)
+    say("gpt2 tiny zero wte")
+    _, loss = _gpu_step(torch, cfg, synth.HP_TINY, params, x, y)
+    assert abs(loss - math.log(cfg.V)) <= 1e-6 * math.log(cfg.V)
+
+
+def test_tiny_step_deterministic():
+    torch = torch_gpu()
+    cfg, params, x, y = tiny_inputs()
+    say("gpt2 tiny determinism")
+    m1, l1 = _gpu_step(torch, cfg, synth.HP_TINY, params, x, y)
+    m2, l2 = _gpu_step(torch, cfg, synth.HP_TINY, params, x, y)
+    assert l1 == l2
+    assert torch.equal(m1.grads, m2.grads) and torch.equal(m1.params, m2.params)
+    assert torch.equal(m1.opt_state, m2.opt_state)
+
+
+def test_tiny_multi_step_losses():
+    torch = torch_gpu()
+    cfg, params, x, y = tiny_inputs()
+    hp = synth.HP_TINY
+    specs = synth.param_specs(cfg)
+    say("gpt2 tiny 3 steps")
+    model = bt.GPT2(cfg, hp, 2, 32)
+    model.load_params(synth.flatten(cfg, params))
+    xd, yd = dev(torch, x), dev(torch, y)
+    p = {k: v.astype(np.float64) for k, v in params.items()}
+    m = {k: np.zeros_like(v) for k, v in p.items()}
+    v = {k: np.zeros_like(val) for k, val in p.items()}
+    for t in range(1, 4):
+        loss = model.train_step(xd, yd)
+        ref = og.train_step(cfg, hp, specs, p, m, v, x, y, t=t)
+        p, m, v = ref["params"], ref["m"], ref["v"]
+        say(f"step {t}: gpu {loss:.8f} oracle {ref['loss']:.8f}")
+        assert abs(loss - ref["loss"]) <= 1e-4 * abs(ref["loss"])
+
+
+def test_tiny_accumulation_equals_large_batch():
+    torch = torch_gpu()
+    cfg = synth.TINY
+    hp = synth.HP_124M  # with clipping
+    specs = synth.param_specs(cfg)
+    params = synth.init_params(cfg, 5)
+    stream = synth.zipf_tokens(8 * 32 + 1, cfg.V, 1.1, 50)
+    x, y = synth.shifted_pair(stream, 8, 32)
+    say("gpt2 tiny accumulation 4 x 2 vs 8")
+    big, loss_big = _gpu_step(torch, cfg, hp, params, x, y)
+    acc = bt.GPT2(cfg, hp, 2, 32)
+    acc.load_params(synth.flatten(cfg, params))
+    d_loss = torch.zeros(1, device="cuda")
+    for k in range(4):
+        acc.fwd_bwd(dev(torch, x[2 * k:2 * k + 2]), dev(torch, y[2 * k:2 * k + 2]), 1.0 / (8 * 32), k > 0, d_loss)
+    acc.optimizer_step(1, hp.lr)
+    torch.cuda.synchronize()
+    assert abs(float(d_loss.item()) - loss_big) <= 1e-6 * abs(loss_big)
+    zeros = {k: np.zeros_like(v, dtype=np.float64) for k, v in params.items()}
+    ref = og.train_step(cfg, hp, specs, params, zeros, zeros, x, y, t=1, accum=4)
+    ga, gb = _unflat(cfg, acc.grads), _unflat(cfg, big.grads)
+    for name, _, _ in specs:
+        assert_close_maxabs(ga[name], gb[name], GRAD_TOL, f"accum vs big {name}")
+        assert_close_maxabs(ga[name], ref["grads"][name], GRAD_TOL, f"accum vs oracle {name}")
+    _check_update(cfg, hp, specs, params, ga, _unflat(cfg, acc.params), _unflat(cfg, acc.m), _unflat(cfg, acc.v), 1,
+                  what="accum")
+
+
+# ---------------------------------------------------------------- GPT-2 124M
+def _inputs_124m(B=16, T=1024):
+    cfg = synth.GPT2_124M
+    params = synth.init_params(cfg, 4)
+    stream = synth.zipf_tokens(B * T + 1, cfg.V, 1.1, 40)
+    x, y = synth.shifted_pair(stream, B, T)
+    return cfg, params, x, y
+
+
+@pytest.mark.timeout(600)
+def test_gpt2_124m_loss_rows_sampled():
+    torch = torch_gpu()
+    cfg, params, x, y = _inputs_124m()
+    hp = synth.HP_124M
+    B, T = x.shape
+    say("gpt2 124M B=16 T=1024 fwd_bwd loss rows")
+    model = bt.GPT2(cfg, hp, B, T)
+    model.load_params(synth.flatten(cfg, params))
+    d_loss = torch.zeros(1, device="cuda")
+    rows = torch.zeros(B * T, device="cuda")
+    model.fwd_bwd(dev(torch, x), dev(torch, y), 1.0 / (B * T), 0, d_loss, rows)
+    lr_gpu = host(rows).reshape(B, T)
+    assert np.isfinite(lr_gpu).all()
+    assert abs(float(d_loss.item()) - lr_gpu.mean()) <= 1e-5 * lr_gpu.mean()
+    for b in (0, 11):
+        say(f"oracle forward of sequence {b}")
+        _, rr, _ = og.forward(cfg, params, x[b:b + 1], y[b:b + 1])
+        err = np.abs(lr_gpu[b] - rr).max() / np.abs(rr).max()
+        say(f"[parity] loss rows seq {b}: max rel {err:.3e}")
+        assert np.allclose(lr_gpu[b], rr, rtol=LOSS_TOL, atol=0)
+
+
+@pytest.mark.timeout(900)
+def test_gpt2_124m_replicated_sequence_full_step():
+    """16 copies of one sequence: the batch-mean gradient equals the
+    one-sequence gradient, so the oracle run on that sequence alone gives
+    every gradient and the clipped AdamW update of the full-size step."""
+    torch = torch_gpu()
+    cfg, params, x, y = _inputs_124m()
+    hp = synth.HP_124M
+    specs = synth.param_specs(cfg)
+    B, T = x.shape
+    xr = np.repeat(x[3:4], B, axis=0)
+    yr = np.repeat(y[3:4], B, axis=0)
+    say("gpt2 124M replicated-sequence train step")
+    model, loss = _gpu_step(torch, cfg, hp, params, xr, yr)
+    g = _unflat(cfg, model.grads)
+    p = _unflat(cfg, model.params)
+    m = _unflat(cfg, model.m)
+    v = _unflat(cfg, model.v)
+    _, norm_gpu, coef_gpu = model.read_scalars()
+    del model
+    say("oracle step on the single sequence")
+    zeros = {k: np.zeros(s, dtype=np.float64) for k, s, _ in specs}
+    ref = og.train_step(cfg, hp, specs, params, zeros, zeros, x[3:4], y[3:4], t=1)
+    say(f"loss gpu={loss:.8f} oracle={ref['loss']:.8f}; norm gpu={norm_gpu:.6f} oracle={ref['norm']:.6f}")
+    assert abs(loss - ref["loss"]) <= LOSS_TOL * abs(ref["loss"])
+    assert abs(norm_gpu - ref["norm"]) <= 1e-4 * ref["norm"]
+    for name, _, _ in specs:
+        assert_close_maxabs(g[name], ref["grads"][name], GRAD_TOL, f"grad {name}")
+    norm, coef = _check_update(cfg, hp, specs, params, g, p, m, v, 1, what="124M")
+    assert abs(coef - coef_gpu) <= 1e-6 * coef
+    _check_end_to_end(hp, specs, params, g, ref["grads"], p, ref["params"])

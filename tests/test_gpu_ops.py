@@ -1,0 +1,209 @@
+"""Parity of the memory-bound kernels against the float64 oracle:
+LayerNorm fwd/bwd, GELU fwd/bwd, sparse cross-entropy (fwd, bwd, fused),
+AdamW, global grad norm + clip, embeddings fwd/bwd and column sums.
+
+Sizes span the GPT-2 124M shapes (16384 rows of 768, 50,304-column logits,
+the 124.5M-element parameter arena) and small ragged ones.  Bars: 1e-5 of
+max-abs for values, 1e-4 of max-abs for gradients of the model, 1e-6 of
+max-abs for the AdamW update on identical inputs; integer/index results and
+the zero gradient of padded columns exactly."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import ops
+from paper_2606_24780_amd import bt, synth
+from tests.gpu_util import assert_close_maxabs, dev, host, say, torch_gpu
+
+pytestmark = pytest.mark.gpu
+RNG = np.random.Generator(np.random.PCG64(4))
+
+
+# ------------------------------------------------------------------ LayerNorm
+@pytest.mark.parametrize("M,C", [(1, 64), (37, 768), (16384, 768), (5, 4096), (9, 1000)])
+def test_layernorm(M, C):
+    torch = torch_gpu()
+    say(f"layernorm M={M} C={C}")
+    x = (RNG.standard_normal((M, C)) * 2 + 0.5).astype(np.float32)
+    g = (1 + 0.1 * RNG.standard_normal(C)).astype(np.float32)
+    b = (0.1 * RNG.standard_normal(C)).astype(np.float32)
+    dy = RNG.standard_normal((M, C)).astype(np.float32)
+    dx0 = RNG.standard_normal((M, C)).astype(np.float32)
+    dg0 = RNG.standard_normal(C).astype(np.float32)
+    db0 = RNG.standard_normal(C).astype(np.float32)
+    xd, gd, bd = dev(torch, x), dev(torch, g), dev(torch, b)
+    y = torch.empty_like(xd)
+    mean = torch.empty(M, device="cuda")
+    rstd = torch.empty(M, device="cuda")
+    bt.bt_layernorm_fwd(xd, gd, bd, y, mean, rstd, M, C, 1e-5)
+    ry, rm, rr = ops.layernorm_fwd(x, g, b, 1e-5)
+    assert_close_maxabs(host(y), ry, 1e-5, "y")
+    assert_close_maxabs(host(mean), rm, 1e-5, "mean")
+    assert_close_maxabs(host(rstd), rr, 1e-5, "rstd")
+    rdx, rdg, rdb = ops.layernorm_bwd(dy, x, g, rm, rr)
+    for beta in (0.0, 1.0):
+        dx, dgd, dbd = dev(torch, dx0), dev(torch, dg0), dev(torch, db0)
+        bt.bt_layernorm_bwd(dev(torch, dy), xd, gd, mean, rstd, dx, dgd, dbd, beta, beta, M, C)
+        assert_close_maxabs(host(dx), rdx + beta * dx0, 1e-5, f"dx beta={beta}")
+        assert_close_maxabs(host(dgd), rdg + beta * dg0, 1e-5, f"dgamma beta={beta}")
+        assert_close_maxabs(host(dbd), rdb + beta * db0, 1e-5, f"dbeta beta={beta}")
+
+
+# ----------------------------------------------------------------------- GELU
+@pytest.mark.parametrize("n", [4, 4 * 1001, 16384 * 3072])
+def test_gelu(n):
+    torch = torch_gpu()
+    say(f"gelu n={n}")
+    x = (RNG.standard_normal(n) * 3).astype(np.float32)
+    dy = RNG.standard_normal(n).astype(np.float32)
+    xd = dev(torch, x)
+    y = torch.empty_like(xd)
+    bt.bt_gelu_fwd(xd, y)
+    assert_close_maxabs(host(y), ops.gelu_fwd(x), 1e-6, "gelu")
+    dyd = dev(torch, dy)
+    bt.bt_gelu_bwd(xd, dyd, dyd)  # in place over dy
+    assert_close_maxabs(host(dyd), ops.gelu_bwd(x, dy), 1e-6, "gelu bwd (in place)")
+
+
+# --------------------------------------------------------------- Cross-entropy
+@pytest.mark.parametrize("M,V,Vp", [(5, 256, 256), (7, 50257, 50304), (3, 13, 16), (2, 1, 4)])
+def test_xent(M, V, Vp):
+    torch = torch_gpu()
+    say(f"xent M={M} V={V} Vp={Vp}")
+    z = (RNG.standard_normal((M, Vp)) * 2).astype(np.float32)
+    y = RNG.integers(0, V, M).astype(np.int32)
+    y[-1] = V - 1
+    scale = 1.0 / (M * 3)
+    zd, yd = dev(torch, z), dev(torch, y)
+    loss = torch.empty(M, device="cuda")
+    lse = torch.empty(M, device="cuda")
+    bt.bt_softmax_xent_fwd(zd, yd, loss, lse, M, V, Vp)
+    rl, rlse = ops.xent_fwd(z, y, V)
+    assert np.allclose(host(loss), rl, rtol=1e-5, atol=1e-5 * max(1.0, np.abs(rl).max()))
+    assert np.allclose(host(lse), rlse, rtol=1e-6, atol=1e-6)
+    rdz = ops.xent_bwd(z, y, V, scale)
+    dz = torch.empty_like(zd)
+    bt.bt_softmax_xent_bwd(zd, lse, yd, dz, scale, M, V, Vp)
+    assert_close_maxabs(host(dz), rdz, 1e-5, "dlogits (bwd)")
+    assert np.all(host(dz)[:, V:] == 0)
+    loss2 = torch.empty(M, device="cuda")
+    lse2 = torch.empty(M, device="cuda")
+    bt.bt_softmax_xent_fused(zd, yd, loss2, lse2, scale, M, V, Vp)  # in place
+    assert np.allclose(host(loss2), rl, rtol=1e-5, atol=1e-5 * max(1.0, np.abs(rl).max()))
+    assert_close_maxabs(host(zd), rdz, 1e-5, "dlogits (fused, in place)")
+    assert np.all(host(zd)[:, V:] == 0)
+    # rows of (softmax - onehot) sum to zero
+    assert np.abs(host(zd)[:, :V].sum(axis=1)).max() <= 1e-6 * scale * 10
+
+
+def test_xent_zero_logits_is_ln_V():
+    torch = torch_gpu()
+    M, V, Vp = 64, 50257, 50304
+    say("xent zero logits")
+    z = torch.zeros((M, Vp), device="cuda")
+    y = dev(torch, RNG.integers(0, V, M).astype(np.int32))
+    loss = torch.empty(M, device="cuda")
+    lse = torch.empty(M, device="cuda")
+    bt.bt_softmax_xent_fwd(z, y, loss, lse, M, V, Vp)
+    assert np.allclose(host(loss), math.log(V), rtol=1e-6, atol=0)
+
+
+def test_xent_full_size_sampled():
+    torch = torch_gpu()
+    M, V, Vp = 16384, 50257, 50304
+    say("xent full size fused")
+    g = torch.Generator(device="cuda").manual_seed(4)
+    z = torch.randn((M, Vp), generator=g, device="cuda") * 3
+    y = dev(torch, synth.zipf_tokens(M, V, 1.1, 40))
+    rows = np.sort(RNG.choice(M, 32, replace=False))
+    zr = host(z[torch.from_numpy(rows).cuda()])
+    loss = torch.empty(M, device="cuda")
+    lse = torch.empty(M, device="cuda")
+    bt.bt_softmax_xent_fused(z, y, loss, lse, 1.0 / M, M, V, Vp)
+    yr = host(y).astype(np.int64)[rows]
+    rl, _ = ops.xent_fwd(zr, yr, V)
+    assert np.allclose(host(loss)[rows], rl, rtol=1e-5, atol=0)
+    assert_close_maxabs(host(z[torch.from_numpy(rows).cuda()]), ops.xent_bwd(zr, yr, V, 1.0 / M), 1e-5,
+                        "dlogits rows")
+
+
+# ---------------------------------------------------------------------- AdamW
+@pytest.mark.parametrize("t,clip", [(1, None), (2, 0.37), (7, None)])
+def test_adamw(t, clip):
+    torch = torch_gpu()
+    n, nd = 4 * 2501, 4 * 1600
+    say(f"adamw t={t} clip={clip}")
+    p = RNG.standard_normal(n).astype(np.float32)
+    g = (RNG.standard_normal(n) * 1e-2).astype(np.float32)
+    g[:5] = 0
+    m = (RNG.standard_normal(n) * 1e-3).astype(np.float32)
+    v = (RNG.random(n) * 1e-5).astype(np.float32)
+    hp = synth.HP_124M
+    pd, gd, md, vd = dev(torch, p), dev(torch, g), dev(torch, m), dev(torch, v)
+    coef = None if clip is None else dev(torch, np.array([clip], np.float32))
+    bt.bt_adamw_step(pd, gd, md, vd, n, nd, hp.lr, hp.beta1, hp.beta2, hp.eps, hp.weight_decay, t, coef)
+    mask = (np.arange(n) < nd).astype(np.float64)
+    rp, rm, rv = ops.adamw(p, g, m, v, t, hp.lr, hp.beta1, hp.beta2, hp.eps, hp.weight_decay, mask,
+                           1.0 if clip is None else float(np.float32(clip)))
+    assert_close_maxabs(host(pd), rp, 1e-6, "p")
+    assert_close_maxabs(host(md), rm, 1e-6, "m")
+    assert_close_maxabs(host(vd), rv, 1e-6, "v")
+
+
+def test_grad_norm_full_arena():
+    torch = torch_gpu()
+    n = synth.num_params(synth.GPT2_124M)
+    say(f"grad norm n={n}")
+    g = torch.Generator(device="cuda").manual_seed(5)
+    x = torch.randn(n, generator=g, device="cuda") * 1e-3
+    out = torch.zeros(2, device="cuda")
+    bt.bt_grad_norm_clip(x, n, 1.0, out[0:1], out[1:2])
+    norm = ops.grad_norm(host(x))
+    o = host(out)
+    assert abs(o[0] - norm) <= 1e-6 * norm
+    assert abs(o[1] - ops.clip_coef(norm, 1.0)) <= 1e-6
+    bt.bt_grad_norm_clip(x * 1e-4, n, 1.0, out[0:1], out[1:2])
+    assert host(out)[1] == 1.0  # norm below the threshold: no clipping
+
+
+# ----------------------------------------------------------------- Embeddings
+@pytest.mark.parametrize("B,T,C,Vp,V", [(2, 32, 64, 256, 256), (16, 1024, 768, 50304, 50257), (3, 7, 12, 20, 17)])
+def test_embedding(B, T, C, Vp, V):
+    torch = torch_gpu()
+    say(f"embedding B={B} T={T} C={C}")
+    wte = RNG.standard_normal((Vp, C)).astype(np.float32)
+    wpe = RNG.standard_normal((T + 3, C)).astype(np.float32)
+    tok = synth.zipf_tokens(B * T, V, 1.1, 9).reshape(B, T)
+    tokd = dev(torch, tok)
+    x0 = torch.empty((B * T, C), device="cuda")
+    bt.bt_embedding_fwd(tokd, dev(torch, wte), dev(torch, wpe), x0, B, T, C, Vp)
+    assert np.array_equal(host(x0), (ops.embedding_fwd(wte, wpe, tok)).reshape(B * T, C).astype(np.float32))
+    dx0 = RNG.standard_normal((B, T, C)).astype(np.float32)
+    dwte0 = RNG.standard_normal((Vp, C)).astype(np.float32)
+    dwpe0 = RNG.standard_normal((T + 3, C)).astype(np.float32)
+    rwte, rwpe = ops.embedding_bwd(dx0, tok, Vp, T + 3)
+    for beta in (0.0, 1.0):
+        dwte = dev(torch, dwte0)
+        dwpe = dev(torch, dwpe0)
+        bt.bt_embedding_bwd(tokd, dev(torch, dx0), dwte, dwpe, beta, B, T, C, Vp)
+        assert_close_maxabs(host(dwte), rwte + dwte0, 1e-5, f"dwte beta={beta}")
+        exp_wpe = dwpe0.astype(np.float64).copy()
+        exp_wpe[:T] = rwpe[:T] + beta * dwpe0[:T]
+        assert_close_maxabs(host(dwpe), exp_wpe, 1e-5, f"dwpe beta={beta}")
+        d2 = dev(torch, dwte0)
+        bt.bt_embedding_bwd(tokd, dev(torch, dx0), d2, dev(torch, dwpe0), beta, B, T, C, Vp)
+        assert torch.equal(d2, dwte), "embedding backward not deterministic"
+
+
+# ---------------------------------------------------------------- Column sums
+@pytest.mark.parametrize("M,N", [(16384, 3072), (37, 20), (1, 4), (16384, 2304)])
+def test_colsum(M, N):
+    torch = torch_gpu()
+    say(f"colsum M={M} N={N}")
+    X = RNG.standard_normal((M, N)).astype(np.float32)
+    o0 = RNG.standard_normal(N).astype(np.float32)
+    for beta in (0.0, 1.0):
+        out = dev(torch, o0)
+        bt.bt_colsum(dev(torch, X), M, N, N, out, beta)
+        assert_close_maxabs(host(out), X.astype(np.float64).sum(0) + beta * o0, 1e-5, f"colsum beta={beta}")
