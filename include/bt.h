@@ -80,6 +80,11 @@ typedef enum {
  * M, N, K >= 0 (an empty product writes beta*C + residual with acc = 0; with
  * K = 0 the epilogue still applies).  M, N, K, lda, ldb, ldc must be
  * multiples of 4.  FP32 inputs, FP32 accumulation on the matrix cores.
+ * colsum_B (optional, [N]) receives the column sums of op(B) over K,
+ *   colsum_B[n] = beta * colsum_B[n] + sum_k op(B)[k, n],
+ * i.e. the bias gradient sum_m dY[m, n] of a weight-gradient product
+ * dW = X^T dY, computed from the dY tiles the product already reads.  It
+ * requires opB = BT_OP_N, epi = BT_EPI_NONE and no residual.
  * ws may be NULL when bt_gemm_ws_bytes() returns 0 for the shape; otherwise
  * it must hold that many bytes (split-K partial products).
  */
@@ -87,7 +92,8 @@ bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K,
                   const float* A, int lda, const float* B, int ldb,
                   float beta, float* C, int ldc,
                   const float* bias, bt_epi epi, float* preact_out, const float* gelu_in,
-                  const float* residual, void* ws, size_t ws_bytes, void* stream);
+                  const float* residual, float* colsum_B, void* ws, size_t ws_bytes,
+                  void* stream);
 size_t bt_gemm_ws_bytes(bt_op opA, bt_op opB, int M, int N, int K, bt_epi epi);
 
 /*
@@ -179,10 +185,13 @@ bt_status bt_softmax_xent_fused(float* logits, const int32_t* targets, float* lo
  * c = *grad_scale (1 if grad_scale is NULL) and d = (i < n_decay):
  *   g = c * g[i];  m = b1 m + (1-b1) g;  v = b2 v + (1-b2) g^2
  *   p = p - lr*wd*d*p - lr * (m / (1-b1^t)) / (sqrt(v / (1-b2^t)) + eps)
- * t >= 1.  n and n_decay multiples of 4, n_decay <= n.
+ * t >= 1.  n and n_decay multiples of 4, n_decay <= n.  The scalars are
+ * host doubles: 1 - beta and the bias corrections are formed in double and
+ * rounded to FP32 once (0.999 itself is not an FP32 number; 1 - 0.999f would
+ * be off by 1.3e-5 relative).
  */
 bt_status bt_adamw_step(float* p, const float* g, float* m, float* v, size_t n, size_t n_decay,
-                        float lr, float beta1, float beta2, float eps, float weight_decay, int t,
+                        double lr, double beta1, double beta2, double eps, double weight_decay, int t,
                         const float* grad_scale, void* stream);
 
 /*
@@ -239,8 +248,8 @@ typedef struct {
   int H;            /* heads; C / H must be 64 */
   int C;            /* model width, multiple of 64 */
   float ln_eps;     /* LayerNorm epsilon */
-  float lr, beta1, beta2, adam_eps, weight_decay;
-  float grad_clip;  /* <= 0: no clipping */
+  double lr, beta1, beta2, adam_eps, weight_decay;  /* AdamW (host scalars) */
+  double grad_clip; /* <= 0: no clipping */
 } bt_gpt2_config;
 
 typedef struct bt_gpt2_ctx bt_gpt2_ctx;
@@ -281,7 +290,7 @@ bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, float* grads,
 /* Global gradient norm, clip (cfg.grad_clip > 0) and AdamW at step t with
  * learning rate lr.  The norm and clip coefficient stay on the device. */
 bt_status bt_gpt2_optimizer_step(bt_gpt2_ctx* ctx, float* params, float* grads, float* opt_state,
-                                 int t, float lr);
+                                 int t, double lr);
 /* Waits for the context's stream, then copies to host out[3] the device
  * scalars [last loss written by bt_gpt2_train_step, gradient norm, clip
  * coefficient] of the last step. */

@@ -47,17 +47,20 @@ class KernelStat(_c.Structure):
                 ("bytes", _c.c_double)]
 
 
+f64 = _c.c_double
+
+
 class GPT2ConfigC(_c.Structure):
     _fields_ = [("V", i32), ("Vp", i32), ("max_T", i32), ("L", i32), ("H", i32), ("C", i32),
-                ("ln_eps", f32), ("lr", f32), ("beta1", f32), ("beta2", f32), ("adam_eps", f32),
-                ("weight_decay", f32), ("grad_clip", f32)]
+                ("ln_eps", f32), ("lr", f64), ("beta1", f64), ("beta2", f64), ("adam_eps", f64),
+                ("weight_decay", f64), ("grad_clip", f64)]
 
 
 _SIGS = {
     "bt_status_str": (_c.c_char_p, [i32]),
     "bt_last_error": (_c.c_char_p, []),
     "bt_version": (_c.c_char_p, []),
-    "bt_gemm": (i32, [i32, i32, i32, i32, i32, vp, i32, vp, i32, f32, vp, i32, vp, i32, vp, vp, vp, vp, sz, vp]),
+    "bt_gemm": (i32, [i32, i32, i32, i32, i32, vp, i32, vp, i32, f32, vp, i32, vp, i32, vp, vp, vp, vp, vp, sz, vp]),
     "bt_gemm_ws_bytes": (sz, [i32, i32, i32, i32, i32, i32]),
     "bt_attention_fwd": (i32, [vp, vp, vp, i32, i32, i32, i32, vp]),
     "bt_attention_bwd": (i32, [vp, vp, vp, vp, vp, vp, sz, i32, i32, i32, i32, vp]),
@@ -70,7 +73,8 @@ _SIGS = {
     "bt_softmax_xent_fwd": (i32, [vp, vp, vp, vp, i32, i32, i32, vp]),
     "bt_softmax_xent_bwd": (i32, [vp, vp, vp, vp, f32, i32, i32, i32, vp]),
     "bt_softmax_xent_fused": (i32, [vp, vp, vp, vp, f32, i32, i32, i32, vp]),
-    "bt_adamw_step": (i32, [vp, vp, vp, vp, sz, sz, f32, f32, f32, f32, f32, i32, vp, vp]),
+    "bt_adamw_step": (i32, [vp, vp, vp, vp, sz, sz, _c.c_double, _c.c_double, _c.c_double, _c.c_double,
+                            _c.c_double, i32, vp, vp]),
     "bt_grad_norm_clip": (i32, [vp, sz, f32, vp, vp, vp, sz, vp]),
     "bt_grad_norm_ws_bytes": (sz, [sz]),
     "bt_embedding_fwd": (i32, [vp, vp, vp, vp, i32, i32, i32, i32, vp]),
@@ -88,7 +92,7 @@ _SIGS = {
     "bt_gpt2_set_step_count": (None, [vp, i32]),
     "bt_gpt2_read_scalars": (i32, [vp, _c.POINTER(f32)]),
     "bt_gpt2_fwd_bwd": (i32, [vp, vp, vp, vp, vp, i32, i32, f32, i32, vp, vp]),
-    "bt_gpt2_optimizer_step": (i32, [vp, vp, vp, vp, i32, f32]),
+    "bt_gpt2_optimizer_step": (i32, [vp, vp, vp, vp, i32, _c.c_double]),
     "bt_gpt2_train_step": (f32, [vp, vp, vp, vp, vp, vp, i32, i32]),
     "bt_gpt2_profile_enable": (i32, [vp, i32]),
     "bt_gpt2_profile_read": (i32, [vp, _c.POINTER(KernelStat), i32]),
@@ -161,13 +165,14 @@ def _ws(nbytes: int, ws=None, device=None):
 
 # ---------------------------------------------------------------- operations
 def bt_gemm(opA, opB, M, N, K, A, lda, B, ldb, beta, C, ldc, bias=None, epi=EPI_NONE,
-            preact_out=None, gelu_in=None, residual=None, ws=None, stream=None):
+            preact_out=None, gelu_in=None, residual=None, colsum_B=None, ws=None, stream=None):
     L = lib()
     need = L.bt_gemm_ws_bytes(opA, opB, M, N, K, epi)
     w = _ws(need, ws, C.device)
     nbytes = 0 if w is None else w.numel() * w.element_size()
     _check(L.bt_gemm(opA, opB, M, N, K, _p(A), lda, _p(B), ldb, beta, _p(C), ldc, _p(bias), epi,
-                     _p(preact_out), _p(gelu_in), _p(residual), _p(w), nbytes, _stream(stream)), "bt_gemm")
+                     _p(preact_out), _p(gelu_in), _p(residual), _p(colsum_B), _p(w), nbytes,
+                     _stream(stream)), "bt_gemm")
     return C
 
 

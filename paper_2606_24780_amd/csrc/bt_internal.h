@@ -29,6 +29,12 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // Zero n floats with a small kernel (no memset node).
 bt_status fill_zero(float* p, size_t n, hipStream_t s);
 
+// Fixed-order sum of per-block partial rows: for c < n,
+//   dst[c] = beta * dst[c] + sum_{b < nb} part[b * ld + c],
+// where dst is out_a[c] for c < n_a and out_b[c - n_a] otherwise.
+bt_status sum_partials(const float* part, int nb, long long ld, int n, float* out_a, int n_a, float* out_b,
+                       float beta, hipStream_t s);
+
 // ------------------------------------------------------------------ device
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
@@ -45,22 +51,39 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
-// tanh-form GELU and its derivative (FP32).
-__device__ __forceinline__ float gelu_f(float x) {
+// tanh-form GELU and its derivative (FP32), evaluated through the logistic
+// function: 1 + tanh(u) = 2 s with s = 1 / (1 + exp(-2u)), so
+//   gelu(x)  = x s
+//   gelu'(x) = s + 2 x s (1 - s) u'(x),   u = sqrt(2/pi) (x + 0.044715 x^3).
+// Both s and 1 - s are formed without cancellation (the exponent is always
+// <= 0), which keeps the tails accurate where 1 +- tanh(u) would round away.
+__device__ __forceinline__ void gelu_logistic(float x, float& s, float& oms, float& du) {
   const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
   const float k1 = 0.044715f;
-  float u = k0 * (x + k1 * x * x * x);
-  return 0.5f * x * (1.0f + tanhf(u));
+  const float x2 = x * x;
+  const float u = k0 * (x + k1 * x2 * x);
+  du = k0 * (1.0f + 3.0f * k1 * x2);
+  const float e = expf(-2.0f * fabsf(u));  // in (0, 1]
+  const float r = 1.0f / (1.0f + e);
+  if (u >= 0.f) {
+    s = r;
+    oms = e * r;
+  } else {
+    s = e * r;
+    oms = r;
+  }
+}
+
+__device__ __forceinline__ float gelu_f(float x) {
+  float s, oms, du;
+  gelu_logistic(x, s, oms, du);
+  return x * s;
 }
 
 __device__ __forceinline__ float gelu_grad_f(float x) {
-  const float k0 = 0.7978845608028654f;
-  const float k1 = 0.044715f;
-  float x2 = x * x;
-  float u = k0 * (x + k1 * x2 * x);
-  float t = tanhf(u);
-  float du = k0 * (1.0f + 3.0f * k1 * x2);
-  return 0.5f * (1.0f + t) + 0.5f * x * (1.0f - t * t) * du;
+  float s, oms, du;
+  gelu_logistic(x, s, oms, du);
+  return s + 2.0f * x * s * oms * du;
 }
 
 }  // namespace bt

@@ -41,7 +41,8 @@ __global__ void __launch_bounds__(EW_THREADS) gelu_bwd_kernel(const floatx4* __r
 }
 
 struct AdamArgs {
-  float lr, beta1, beta2, eps, wd;
+  float lr, beta1, beta2, eps, lr_wd;
+  float omb1, omb2;        // 1 - beta1, 1 - beta2, rounded once from double
   float inv_bc1, inv_bc2;  // 1/(1-beta1^t), 1/(1-beta2^t)
 };
 
@@ -52,12 +53,12 @@ __global__ void __launch_bounds__(EW_THREADS) adamw_kernel(floatx4* __restrict__
   const float c = grad_scale ? *grad_scale : 1.f;
   for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (size_t)gridDim.x * blockDim.x) {
     floatx4 pp = p[i], gg = g[i], mm = m[i], vv = v[i];
-    const float dec = i < nd4 ? a.lr * a.wd : 0.f;
+    const float dec = i < nd4 ? a.lr_wd : 0.f;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const float gk = gg[k] * c;
-      mm[k] = a.beta1 * mm[k] + (1.f - a.beta1) * gk;
-      vv[k] = a.beta2 * vv[k] + (1.f - a.beta2) * gk * gk;
+      mm[k] = a.beta1 * mm[k] + a.omb1 * gk;
+      vv[k] = a.beta2 * vv[k] + a.omb2 * (gk * gk);
       const float mhat = mm[k] * a.inv_bc1;
       const float vhat = vv[k] * a.inv_bc2;
       pp[k] = pp[k] - dec * pp[k] - a.lr * mhat / (sqrtf(vhat) + a.eps);
@@ -121,19 +122,10 @@ __global__ void __launch_bounds__(EW_THREADS) colsum_partial_kernel(const float*
   const int r1 = min(M, r0 + rpb);
   for (int c = threadIdx.x; c < N4; c += blockDim.x) {
     floatx4 s = floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
     for (int r = r0; r < r1; ++r) s += *reinterpret_cast<const floatx4*>(X + (long long)r * ldx + 4 * c);
     *reinterpret_cast<floatx4*>(part + (long long)blockIdx.x * N + 4 * c) = s;
   }
-}
-
-__global__ void __launch_bounds__(EW_THREADS) colsum_finish_kernel(const float* __restrict__ part, int nparts,
-                                                                   int N, float* __restrict__ out, float beta) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= N) return;
-  float s = 0.f;
-  for (int b = 0; b < nparts; ++b) s += part[(long long)b * N + c];
-  if (beta != 0.f) s += out[c];
-  out[c] = s;
 }
 
 int colsum_blocks(int M) {
@@ -178,6 +170,46 @@ bt_status fill_zero(float* p, size_t n, hipStream_t s) {
   return check_launch("fill_zero_kernel");
 }
 
+// 256 threads = 32 columns x 8 chains; chain g sums partials g, g+8, ...
+// with 8 loads in flight, then the 8 chains are added in order.
+__global__ void __launch_bounds__(256) sum_partials_kernel(const float* __restrict__ part, int nb, long long ld,
+                                                           int n, float* out_a, int n_a, float* out_b,
+                                                           float beta) {
+  __shared__ float red[8][33];
+  const int lane = threadIdx.x & 31, g = threadIdx.x >> 5;
+  const int c = blockIdx.x * 32 + lane;
+  float s = 0.f;
+  if (c < n) {
+    int b = g;
+    for (; b + 56 < nb; b += 64) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = part[(long long)(b + 8 * u) * ld + c];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; b < nb; b += 8) s += part[(long long)b * ld + c];
+  }
+  red[g][lane] = s;
+  __syncthreads();
+  if (g == 0 && c < n) {
+    float t = red[0][lane];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) t += red[k][lane];
+    float* d = c < n_a ? out_a + c : out_b + (c - n_a);
+    if (beta != 0.f) t += *d;
+    *d = t;
+  }
+}
+
+bt_status sum_partials(const float* part, int nb, long long ld, int n, float* out_a, int n_a, float* out_b,
+                       float beta, hipStream_t s) {
+  if (n <= 0) return BT_OK;
+  hipLaunchKernelGGL(sum_partials_kernel, dim3((n + 31) / 32), dim3(256), 0, s, part, nb, ld, n, out_a, n_a, out_b,
+                     beta);
+  return check_launch("sum_partials_kernel");
+}
+
 bt_status launch_loss_sum(const float* rows, int n, float scale, int accumulate, float* d_loss, hipStream_t s) {
   hipLaunchKernelGGL(loss_sum_kernel, dim3(1), dim3(256), 0, s, rows, n, scale, accumulate, d_loss);
   return check_launch("loss_sum_kernel");
@@ -212,25 +244,27 @@ extern "C" bt_status bt_gelu_bwd(const float* x, const float* dy, float* dx, siz
 }
 
 extern "C" bt_status bt_adamw_step(float* p, const float* g, float* m, float* v, size_t n, size_t n_decay,
-                                   float lr, float beta1, float beta2, float eps, float weight_decay, int t,
+                                   double lr, double beta1, double beta2, double eps, double weight_decay, int t,
                                    const float* grad_scale, void* stream) {
   BT_RETURN_IF((n & 3) || (n_decay & 3) || n_decay > n, BT_ESHAPE,
                "bt_adamw_step: n=%zu, n_decay=%zu must be multiples of 4 with n_decay <= n", n, n_decay);
   BT_RETURN_IF(t < 1, BT_EINVAL, "bt_adamw_step: step t=%d must be >= 1", t);
-  BT_RETURN_IF(!(beta1 >= 0.f && beta1 < 1.f && beta2 >= 0.f && beta2 < 1.f), BT_EINVAL,
+  BT_RETURN_IF(!(beta1 >= 0.0 && beta1 < 1.0 && beta2 >= 0.0 && beta2 < 1.0), BT_EINVAL,
                "bt_adamw_step: betas must be in [0, 1)");
   if (n == 0) return BT_OK;
   BT_RETURN_IF(!p || !g || !m || !v, BT_EINVAL, "bt_adamw_step: NULL pointer");
   BT_RETURN_IF(!aligned16(p) || !aligned16(g) || !aligned16(m) || !aligned16(v), BT_EALIGN,
                "bt_adamw_step: pointers must be 16-byte aligned");
   AdamArgs a;
-  a.lr = lr;
-  a.beta1 = beta1;
-  a.beta2 = beta2;
-  a.eps = eps;
-  a.wd = weight_decay;
-  a.inv_bc1 = (float)(1.0 / (1.0 - pow((double)beta1, (double)t)));
-  a.inv_bc2 = (float)(1.0 / (1.0 - pow((double)beta2, (double)t)));
+  a.lr = (float)lr;
+  a.beta1 = (float)beta1;
+  a.beta2 = (float)beta2;
+  a.eps = (float)eps;
+  a.lr_wd = (float)(lr * weight_decay);
+  a.omb1 = (float)(1.0 - beta1);
+  a.omb2 = (float)(1.0 - beta2);
+  a.inv_bc1 = (float)(1.0 / (1.0 - pow(beta1, (double)t)));
+  a.inv_bc2 = (float)(1.0 / (1.0 - pow(beta2, (double)t)));
   const size_t n4 = n / 4;
   hipLaunchKernelGGL(adamw_kernel, dim3(ew_blocks(n4)), dim3(EW_THREADS), 0, as_stream(stream),
                      reinterpret_cast<floatx4*>(p), reinterpret_cast<const floatx4*>(g),
@@ -288,6 +322,5 @@ extern "C" bt_status bt_colsum(const float* X, int M, int N, int ldx, float* out
   float* part = static_cast<float*>(ws);
   hipLaunchKernelGGL(colsum_partial_kernel, dim3(nb), dim3(EW_THREADS), 0, s, X, M, N, (long long)ldx, rpb, part);
   BT_TRY(check_launch("colsum_partial_kernel"));
-  hipLaunchKernelGGL(colsum_finish_kernel, dim3((N + 255) / 256), dim3(256), 0, s, part, nb, N, out, beta);
-  return check_launch("colsum_finish_kernel");
+  return sum_partials(part, nb, N, N, out, N, nullptr, beta, s);
 }

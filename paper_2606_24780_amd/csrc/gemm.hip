@@ -7,14 +7,16 @@
 // gradient dW = X^T dY (TN, reduction over tokens, split along K).
 //
 // Design (gfx950):
-//  * block tile 128 x 128 x 32, 256 threads = 4 waves in a 2 x 2 grid, each
-//    wave owns a 64 x 64 sub-tile = 2 x 2 MFMA 32x32 accumulators (64 VGPRs).
+//  * block tile 128 x 128 x BK (BK = 32 at 2 blocks per CU, or BK = 16 at 3-4
+//    blocks per CU for shapes whose tile count would leave CUs with a lone
+//    block), 256 threads = 4 waves in a 2 x 2 grid, each wave owns a 64 x 64
+//    sub-tile = 2 x 2 MFMA 32x32 accumulators (64 VGPRs).
 //  * each operand tile is staged global -> VGPR -> LDS with float4 accesses in
 //    the layout of its source (K-contiguous rows [rows][BK+4] or
 //    MN-contiguous rows [BK][128+4]); two LDS buffers, one barrier per k-tile,
 //    the next tile's global loads in flight while the MFMAs run.
 //  * the MFMA k-slot of lane half h at step s is k = 8h + (s mod 8) +
-//    16 (s div 8): K-contiguous tiles are read as float4 (4 steps at once),
+//    16 (s div 8) (s < BK/2): K-contiguous tiles are read as float4 (4 steps at once),
 //    MN-contiguous tiles as b32 with the two lane halves 8 rows apart, which
 //    keeps both reads free of LDS bank conflicts.
 //  * blocks are remapped so that each XCD (round-robin dispatch over 8 XCDs,
@@ -22,18 +24,23 @@
 //    tile order, so concurrently running tiles share A rows / B columns in L2.
 //  * low-parallelism weight-gradient shapes (small M x N, long K) are split
 //    along K; partials go to a workspace and are summed in a fixed order.
+//    Tile depth, occupancy and split count are chosen per shape from a model
+//    of how the blocks land on the 256 CUs (blocks per CU, resident blocks).
 //  * fused epilogues: bias, bias + tanh-GELU (optionally storing the
 //    pre-activation), GELU-backward (multiply by gelu'(pre)), residual add and
 //    beta = 1 accumulation.
+//  * the weight-gradient product can also return the column sums of dY (the
+//    bias gradient) from the B tiles it already stages, so the bias gradient
+//    costs no extra pass over dY.
 #include "bt_internal.h"
 
 namespace bt {
 namespace {
 
-constexpr int BM = 128, BN = 128, BK = 32;
-constexpr int LDK = BK + 4;   // row stride of K-contiguous LDS tiles
+constexpr int BM = 128, BN = 128;
 constexpr int LDM = BM + 4;   // row stride of MN-contiguous LDS tiles (BM == BN)
 constexpr int NTHREADS = 256;
+constexpr int NUM_CU = 256;
 
 struct GemmParams {
   const float* A;
@@ -44,6 +51,8 @@ struct GemmParams {
   const float* gelu_in;
   const float* residual;
   float* ws;
+  float* colsum;     // optional column sums of op(B) over K (bias gradient of a weight-gradient product)
+  float* ws_colsum;  // split-K partial column sums [splits][N]
   long long lda, ldb, ldc;
   int M, N, K;
   int ksplit;   // K range handled by one split (multiple of BK)
@@ -52,23 +61,24 @@ struct GemmParams {
   float beta;
 };
 
-template <bool KC>
+template <bool KC, int BK>
 struct TileSize {
-  static constexpr int value = KC ? BM * LDK : BK * LDM;
+  static constexpr int value = KC ? BM * (BK + 4) : BK * LDM;
 };
 
-// Global -> register staging of one 128 x 32 operand tile (4 float4 per thread).
-// rows = M (or N) extent, kbeg/kend = k range of this split.
-template <bool KC>
-__device__ __forceinline__ void load_tile(floatx4 (&r)[4], const float* __restrict__ X,
+// Global -> register staging of one 128 x BK operand tile (BK/8 float4 per
+// thread).  rows = M (or N) extent, kbeg/kend = k range of this split.
+template <bool KC, int BK>
+__device__ __forceinline__ void load_tile(floatx4 (&r)[BK / 8], const float* __restrict__ X,
                                           long long ld, int row0, int rows, int k0, int kend,
                                           int tid) {
   if (KC) {
-    // [rows][K]: thread -> (row = tid/8 + 32 i, k = 4 (tid%8)); 128 B per row segment
-    const int kk = k0 + 4 * (tid & 7);
+    // [rows][K]: BK/4 threads per row, 4 consecutive k each (BK*4 bytes per row)
+    constexpr int TPR = BK / 4, RPP = NTHREADS / TPR;
+    const int kk = k0 + 4 * (tid % TPR);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int row = row0 + (tid >> 3) + 32 * i;
+    for (int i = 0; i < BK / 8; ++i) {
+      const int row = row0 + tid / TPR + RPP * i;
       if (row < rows && kk < kend)
         r[i] = *reinterpret_cast<const floatx4*>(X + (long long)row * ld + kk);
       else
@@ -78,7 +88,7 @@ __device__ __forceinline__ void load_tile(floatx4 (&r)[4], const float* __restri
     // [K][rows]: thread -> (k = tid/32 + 8 i, col = 4 (tid%32)); 512 B per k row
     const int col = row0 + 4 * (tid & 31);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < BK / 8; ++i) {
       const int kk = k0 + (tid >> 5) + 8 * i;
       if (kk < kend && col < rows)
         r[i] = *reinterpret_cast<const floatx4*>(X + (long long)kk * ld + col);
@@ -88,24 +98,25 @@ __device__ __forceinline__ void load_tile(floatx4 (&r)[4], const float* __restri
   }
 }
 
-template <bool KC>
-__device__ __forceinline__ void store_tile(float* __restrict__ s, const floatx4 (&r)[4], int tid) {
+template <bool KC, int BK>
+__device__ __forceinline__ void store_tile(float* __restrict__ s, const floatx4 (&r)[BK / 8], int tid) {
   if (KC) {
+    constexpr int TPR = BK / 4, RPP = NTHREADS / TPR;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      *reinterpret_cast<floatx4*>(s + ((tid >> 3) + 32 * i) * LDK + 4 * (tid & 7)) = r[i];
+    for (int i = 0; i < BK / 8; ++i)
+      *reinterpret_cast<floatx4*>(s + (tid / TPR + RPP * i) * (BK + 4) + 4 * (tid % TPR)) = r[i];
   } else {
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < BK / 8; ++i)
       *reinterpret_cast<floatx4*>(s + ((tid >> 5) + 8 * i) * LDM + 4 * (tid & 31)) = r[i];
   }
 }
 
 // Fragment for 4 consecutive MFMA steps (chunk c) of one 32-row block.
-template <bool KC>
+template <bool KC, int BK>
 __device__ __forceinline__ floatx4 read_frag(const float* __restrict__ s, int row, int koff) {
   if (KC) {
-    return *reinterpret_cast<const floatx4*>(s + row * LDK + koff);
+    return *reinterpret_cast<const floatx4*>(s + row * (BK + 4) + koff);
   } else {
     floatx4 v;
     v[0] = s[(koff + 0) * LDM + row];
@@ -134,10 +145,12 @@ __device__ __forceinline__ void epilogue_store(const GemmParams& p, int i, int j
   p.C[off] = v;
 }
 
-template <bool A_KC, bool B_KC, int EPI, bool SPLIT>
-__global__ void __launch_bounds__(NTHREADS, 2) gemm_f32_mfma(const GemmParams p) {
-  constexpr int A_SZ = TileSize<A_KC>::value;
-  constexpr int B_SZ = TileSize<B_KC>::value;
+template <bool A_KC, bool B_KC, int EPI, bool SPLIT, bool COLSUM, int BK, int OCC>
+__global__ void __launch_bounds__(NTHREADS, OCC) gemm_f32_mfma(const GemmParams p) {
+  constexpr int A_SZ = TileSize<A_KC, BK>::value;
+  constexpr int B_SZ = TileSize<B_KC, BK>::value;
+  constexpr int NLD = BK / 8;  // float4 staged per thread per operand
+  static_assert(2 * (A_SZ + B_SZ) * 4 * OCC <= 160 * 1024, "LDS exceeds one CU at this occupancy");
   __shared__ __attribute__((aligned(16))) float smem[2 * (A_SZ + B_SZ)];
 
   const int tid = threadIdx.x;
@@ -175,12 +188,19 @@ __global__ void __launch_bounds__(NTHREADS, 2) gemm_f32_mfma(const GemmParams p)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-  floatx4 ra[4], rb[4];
+  floatx4 ra[NLD], rb[NLD];
+  // Column sums of op(B) (only for MN-contiguous B, i.e. op(B) = B [K][N]):
+  // each thread adds up the B rows it stages, the 8 row groups are combined
+  // at the end.  Only the first tile row of blocks (tm == 0) keeps them.
+  floatx4 csum = floatx4{0.f, 0.f, 0.f, 0.f};
   if (nk > 0) {
-    load_tile<A_KC>(ra, p.A, p.lda, m0, p.M, kbeg, kend, tid);
-    load_tile<B_KC>(rb, p.B, p.ldb, n0, p.N, kbeg, kend, tid);
-    store_tile<A_KC>(smem, ra, tid);
-    store_tile<B_KC>(smem + A_SZ, rb, tid);
+    load_tile<A_KC, BK>(ra, p.A, p.lda, m0, p.M, kbeg, kend, tid);
+    load_tile<B_KC, BK>(rb, p.B, p.ldb, n0, p.N, kbeg, kend, tid);
+    if (COLSUM)
+#pragma unroll
+      for (int i = 0; i < NLD; ++i) csum += rb[i];
+    store_tile<A_KC, BK>(smem, ra, tid);
+    store_tile<B_KC, BK>(smem + A_SZ, rb, tid);
   }
   __syncthreads();
 
@@ -189,19 +209,19 @@ __global__ void __launch_bounds__(NTHREADS, 2) gemm_f32_mfma(const GemmParams p)
     const bool more = kt + 1 < nk;
     if (more) {
       const int k0 = kbeg + (kt + 1) * BK;
-      load_tile<A_KC>(ra, p.A, p.lda, m0, p.M, k0, kend, tid);
-      load_tile<B_KC>(rb, p.B, p.ldb, n0, p.N, k0, kend, tid);
+      load_tile<A_KC, BK>(ra, p.A, p.lda, m0, p.M, k0, kend, tid);
+      load_tile<B_KC, BK>(rb, p.B, p.ldb, n0, p.N, k0, kend, tid);
     }
     const float* sA = smem + cur * (A_SZ + B_SZ);
     const float* sB = sA + A_SZ;
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
+    for (int c = 0; c < BK / 8; ++c) {
       const int koff = 8 * hh + 4 * (c & 1) + 16 * (c >> 1);
       floatx4 fa[2], fb[2];
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) fa[mb] = read_frag<A_KC>(sA, wm * 64 + mb * 32 + lr, koff);
+      for (int mb = 0; mb < 2; ++mb) fa[mb] = read_frag<A_KC, BK>(sA, wm * 64 + mb * 32 + lr, koff);
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb) fb[nb] = read_frag<B_KC>(sB, wn * 64 + nb * 32 + lr, koff);
+      for (int nb = 0; nb < 2; ++nb) fb[nb] = read_frag<B_KC, BK>(sB, wn * 64 + nb * 32 + lr, koff);
 #pragma unroll
       for (int q = 0; q < 4; ++q)
 #pragma unroll
@@ -212,11 +232,36 @@ __global__ void __launch_bounds__(NTHREADS, 2) gemm_f32_mfma(const GemmParams p)
                                                                0, 0, 0);
     }
     if (more) {
+      if (COLSUM)
+#pragma unroll
+        for (int i = 0; i < NLD; ++i) csum += rb[i];
       float* sN = smem + (cur ^ 1) * (A_SZ + B_SZ);
-      store_tile<A_KC>(sN, ra, tid);
-      store_tile<B_KC>(sN + A_SZ, rb, tid);
+      store_tile<A_KC, BK>(sN, ra, tid);
+      store_tile<B_KC, BK>(sN + A_SZ, rb, tid);
     }
     __syncthreads();
+  }
+
+  if (COLSUM && tm == 0) {
+    // combine the 8 staging row groups (tid / 32) in a fixed order
+    floatx4* red = reinterpret_cast<floatx4*>(smem);
+    red[tid] = csum;
+    __syncthreads();
+    if (tid < 32) {
+      floatx4 s = red[tid];
+#pragma unroll
+      for (int gi = 1; gi < 8; ++gi) s += red[tid + 32 * gi];
+      const int n = n0 + 4 * tid;
+      if (n < p.N) {
+        if (SPLIT) {
+          *reinterpret_cast<floatx4*>(p.ws_colsum + (long long)z * p.N + n) = s;
+        } else {
+          floatx4* d = reinterpret_cast<floatx4*>(p.colsum + n);
+          if (p.beta != 0.f) s += *d;
+          *d = s;
+        }
+      }
+    }
   }
 
   // ---- epilogue.  Accumulator element r of lane (lr, hh) of block (mb, nb):
@@ -258,46 +303,106 @@ __global__ void __launch_bounds__(256) splitk_reduce(const float* __restrict__ w
   }
 }
 
-template <bool A_KC, bool B_KC>
-void launch_epi(const GemmParams& p, int epi, bool split, dim3 grid, hipStream_t s) {
+// colsum = sum_z ws_colsum[z] + beta * colsum, fixed order.
+__global__ void __launch_bounds__(256) splitk_colsum_reduce(const float* __restrict__ part, float* __restrict__ out,
+                                                            int N, int splits, float beta) {
+  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= N) return;
+  float s = part[n];
+  for (int z = 1; z < splits; ++z) s += part[(long long)z * N + n];
+  if (beta != 0.f) s += out[n];
+  out[n] = s;
+}
+
+struct GemmCfg {
+  int bk, occ, splits, ksplit;
+};
+
+// Blocks per CU that can stay resident for a layout and tile depth.
+int occupancy_for(int bk, bool akc, bool bkc) {
+  if (bk == 32) return 2;
+  return (akc && bkc) ? 3 : 4;  // two K-contiguous 128 x 20 tiles need 41 KB
+}
+
+// Relative time of a launch of `blocks` equal blocks (each `work` long): the
+// busiest CU holds ceil(blocks / NUM_CU) of them and runs up to `occ` at
+// once; a lone resident 4-wave block keeps the matrix pipe only partly busy
+// (taken as 60%).
+double launch_time(long long blocks, int occ, double work) {
+  const long long per_cu = (blocks + NUM_CU - 1) / NUM_CU;
+  const long long full = per_cu / occ, rem = per_cu % occ;
+  double t = (double)(full * occ) * work;
+  if (rem) t += (double)rem * work / (rem >= 2 ? 1.0 : 0.6);
+  return t;
+}
+
+// Tile depth, occupancy and K split for a shape.  Split-K (only for products
+// without an epilogue) adds a partial-tile round trip through the workspace.
+GemmCfg choose_config(int M, int N, int K, bool akc, bool bkc, bool may_split) {
+  if (K <= 0) return GemmCfg{32, 2, 1, 32};
+  const long long tiles = (long long)((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+  GemmCfg best{32, 2, 1, K};
+  double best_t = 1e300;
+  for (int bk : {32, 16}) {
+    const int occ = occupancy_for(bk, akc, bkc);
+    const int kt = (K + bk - 1) / bk;
+    int smax = 1;
+    if (may_split && tiles < 2LL * NUM_CU * occ && K >= 8 * bk) smax = kt / 4 < 32 ? kt / 4 : 32;
+    for (int s = 1; s <= smax; ++s) {
+      int ks = (K + s - 1) / s;
+      ks = (ks + bk - 1) / bk * bk;
+      if ((K + ks - 1) / ks != s) continue;
+      // time in 128 x 128 x 16 tile steps.  Measured on MI355X: with a
+      // K-contiguous operand, BK = 16 at 3-4 resident blocks runs each step
+      // about 5% faster than BK = 32 at 2 (more waves hide the barriers);
+      // with both operands MN-contiguous the gain is about 2%.
+      const double work = (double)ks / 16.0 * (bk == 16 ? ((akc || bkc) ? 0.95 : 0.98) : 1.0);
+      double t = launch_time(tiles * s, occ, work);
+      if (s > 1) t += 4.0 * (double)s * tiles / NUM_CU;  // partial tiles out and back
+      if (t < best_t * 0.995) {
+        best_t = t;
+        best = GemmCfg{bk, occ, s, ks};
+      }
+    }
+  }
+  return best;
+}
+
+template <bool A_KC, bool B_KC, int BK, int OCC>
+void launch_cfg(const GemmParams& p, int epi, bool split, dim3 grid, hipStream_t s) {
+  const bool cs = p.colsum != nullptr;
   if (split) {
-    hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true>), grid, dim3(NTHREADS), 0, s, p);
+    if (cs)
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, !B_KC, BK, OCC>), grid, dim3(NTHREADS), 0, s, p);
+    else
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, false, BK, OCC>), grid, dim3(NTHREADS), 0, s, p);
     return;
   }
   switch (epi) {
     case BT_EPI_NONE:
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false>), grid, dim3(NTHREADS), 0, s, p);
+      if (cs)
+        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, !B_KC, BK, OCC>), grid, dim3(NTHREADS), 0, s, p);
+      else
+        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, false, BK, OCC>), grid, dim3(NTHREADS), 0, s, p);
       break;
     case BT_EPI_BIAS:
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS, false>), grid, dim3(NTHREADS), 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS, false, false, BK, OCC>), grid, dim3(NTHREADS), 0, s, p);
       break;
     case BT_EPI_BIAS_GELU:
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS_GELU, false>), grid, dim3(NTHREADS), 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS_GELU, false, false, BK, OCC>), grid, dim3(NTHREADS), 0, s, p);
       break;
     default:
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_DGELU, false>), grid, dim3(NTHREADS), 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_DGELU, false, false, BK, OCC>), grid, dim3(NTHREADS), 0, s, p);
       break;
   }
 }
 
-// Number of K splits for a shape: only when the tile grid cannot fill the
-// chip (fewer than 2 blocks per CU on 256 CUs) and K is long.
-int choose_splits(int M, int N, int K, int* ksplit) {
-  const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-  int splits = 1;
-  if (tiles < 512 && K >= 8 * BK) {
-    splits = (512 + tiles - 1) / tiles;
-    const int max_splits = K / (4 * BK);  // at least 4 k-tiles per split
-    if (splits > max_splits) splits = max_splits;
-    if (splits > 32) splits = 32;
-    if (splits < 1) splits = 1;
-  }
-  int ks = (K + splits - 1) / splits;
-  ks = (ks + BK - 1) / BK * BK;
-  if (ks < BK) ks = BK;
-  splits = K > 0 ? (K + ks - 1) / ks : 1;
-  *ksplit = ks;
-  return splits;
+template <bool A_KC, bool B_KC>
+void launch_layout(const GemmParams& p, const GemmCfg& c, int epi, bool split, dim3 grid, hipStream_t s) {
+  if (c.bk == 32)
+    launch_cfg<A_KC, B_KC, 32, 2>(p, epi, split, grid, s);
+  else
+    launch_cfg<A_KC, B_KC, 16, (A_KC && B_KC) ? 3 : 4>(p, epi, split, grid, s);
 }
 
 }  // namespace
@@ -306,19 +411,17 @@ int choose_splits(int M, int N, int K, int* ksplit) {
 using namespace bt;
 
 extern "C" size_t bt_gemm_ws_bytes(bt_op opA, bt_op opB, int M, int N, int K, bt_epi epi) {
-  (void)opA;
-  (void)opB;
   if (M <= 0 || N <= 0 || K <= 0 || epi != BT_EPI_NONE) return 0;
-  int ks;
-  const int splits = choose_splits(M, N, K, &ks);
+  const GemmCfg c = choose_config(M, N, K, opA == BT_OP_N, opB == BT_OP_T, true);
+  const int splits = c.splits;
   if (splits <= 1) return 0;
-  return (size_t)splits * M * N * sizeof(float);
+  return (size_t)splits * ((size_t)M * N + N) * sizeof(float);
 }
 
 extern "C" bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K, const float* A, int lda,
                              const float* B, int ldb, float beta, float* C, int ldc,
                              const float* bias, bt_epi epi, float* preact_out,
-                             const float* gelu_in, const float* residual, void* ws,
+                             const float* gelu_in, const float* residual, float* colsum_B, void* ws,
                              size_t ws_bytes, void* stream) {
   BT_RETURN_IF(opA != BT_OP_N && opA != BT_OP_T, BT_EINVAL, "bt_gemm: bad opA %d", (int)opA);
   BT_RETURN_IF(opB != BT_OP_N && opB != BT_OP_T, BT_EINVAL, "bt_gemm: bad opB %d", (int)opB);
@@ -341,6 +444,9 @@ extern "C" bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K, const fl
                "bt_gemm: bias required for this epilogue");
   BT_RETURN_IF(epi == BT_EPI_DGELU && !gelu_in, BT_EINVAL, "bt_gemm: gelu_in required for DGELU");
   BT_RETURN_IF(residual && residual == C, BT_EINVAL, "bt_gemm: residual must not alias C");
+  BT_RETURN_IF(colsum_B && (opB != BT_OP_N || epi != BT_EPI_NONE || residual), BT_EINVAL,
+               "bt_gemm: colsum_B needs opB = N, no epilogue and no residual");
+  BT_RETURN_IF(colsum_B && !aligned16(colsum_B), BT_EALIGN, "bt_gemm: colsum_B must be 16-byte aligned");
 
   GemmParams p{};
   p.A = A;
@@ -350,6 +456,7 @@ extern "C" bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K, const fl
   p.preact = epi == BT_EPI_BIAS_GELU ? preact_out : nullptr;
   p.gelu_in = gelu_in;
   p.residual = residual;
+  p.colsum = colsum_B;
   p.lda = lda;
   p.ldb = ldb;
   p.ldc = ldc;
@@ -359,34 +466,30 @@ extern "C" bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K, const fl
   p.beta = beta;
   p.tiles_m = (M + BM - 1) / BM;
   p.tiles_n = (N + BN - 1) / BN;
-  int ks = K;
-  int splits = 1;
   const bool may_split = epi == BT_EPI_NONE && residual == nullptr;
-  if (may_split && K > 0) splits = choose_splits(M, N, K, &ks);
-  if (splits <= 1) {
-    splits = 1;
-    ks = K > 0 ? K : BK;
-  }
-  p.ksplit = ks;
+  const bool akc = opA == BT_OP_N;
+  const bool bkc = opB == BT_OP_T;
+  const GemmCfg cfg = choose_config(M, N, K, akc, bkc, may_split);
+  const int splits = cfg.splits;
+  p.ksplit = cfg.ksplit;
   p.splits = splits;
   const bool split = splits > 1;
   if (split) {
-    const size_t need = (size_t)splits * M * N * sizeof(float);
+    const size_t need = (size_t)splits * ((size_t)M * N + N) * sizeof(float);
     BT_RETURN_IF(!ws || ws_bytes < need, BT_EWORKSPACE,
                  "bt_gemm: workspace of %zu bytes needed (got %zu)", need, ws_bytes);
     BT_RETURN_IF(!aligned16(ws), BT_EALIGN, "bt_gemm: workspace must be 16-byte aligned");
     p.ws = static_cast<float*>(ws);
+    p.ws_colsum = p.ws + (size_t)splits * M * N;
   }
   const long long nblocks = (long long)p.tiles_m * p.tiles_n * splits;
   BT_RETURN_IF(nblocks > 0x7fffffffLL, BT_ESHAPE, "bt_gemm: too many tiles");
   dim3 grid((unsigned)nblocks);
   hipStream_t s = as_stream(stream);
-  const bool akc = opA == BT_OP_N;
-  const bool bkc = opB == BT_OP_T;
-  if (akc && !bkc) launch_epi<true, false>(p, epi, split, grid, s);
-  else if (akc && bkc) launch_epi<true, true>(p, epi, split, grid, s);
-  else if (!akc && !bkc) launch_epi<false, false>(p, epi, split, grid, s);
-  else launch_epi<false, true>(p, epi, split, grid, s);
+  if (akc && !bkc) launch_layout<true, false>(p, cfg, epi, split, grid, s);
+  else if (akc && bkc) launch_layout<true, true>(p, cfg, epi, split, grid, s);
+  else if (!akc && !bkc) launch_layout<false, false>(p, cfg, epi, split, grid, s);
+  else launch_layout<false, true>(p, cfg, epi, split, grid, s);
   BT_TRY(check_launch("gemm_f32_mfma"));
   if (split) {
     const long long n4 = (long long)M * (N / 4);
@@ -395,6 +498,11 @@ extern "C" bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K, const fl
     hipLaunchKernelGGL(splitk_reduce, dim3((unsigned)nb), dim3(256), 0, s, p.ws, C, (long long)ldc, M,
                        N, splits, beta);
     BT_TRY(check_launch("splitk_reduce"));
+    if (colsum_B) {
+      hipLaunchKernelGGL(splitk_colsum_reduce, dim3((N + 255) / 256), dim3(256), 0, s, p.ws_colsum, colsum_B, N,
+                         splits, beta);
+      BT_TRY(check_launch("splitk_colsum_reduce"));
+    }
   }
   return BT_OK;
 }

@@ -112,7 +112,7 @@ size_t scratch_need(const bt_gpt2_config& c, int B, int T) {
   mx(bt_gemm_ws_bytes(BT_OP_N, BT_OP_T, M, C, F, BT_EPI_NONE));
   // a split product never needs more than (512 + tiles) tiles of 128 x 128
   // partials with tiles < 512, whatever the token count of the call
-  mx((size_t)1024 * 128 * 128 * sizeof(float));
+  mx((size_t)1024 * 128 * 128 * sizeof(float) + (size_t)64 * (F > 3 * C ? F : 3 * C) * sizeof(float));
   mx(bt_attention_bwd_ws_bytes(B, T, c.H, C / c.H));
   mx(bt_layernorm_bwd_ws_bytes(M, C));
   mx(bt_colsum_ws_bytes(M, F > 3 * C ? F : 3 * C));
@@ -397,23 +397,23 @@ extern "C" bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, floa
     BT_PROF(BT_PROF_LN_FWD, 0, ln_fwd_b, bt_layernorm_fwd(sb.res(l), P + w.ln1g, P + w.ln1b, ln1, sb.layer(ly.mu1, l), sb.layer(ly.rs1, l), M, C,
                             cf.ln_eps, s));
     BT_PROF(BT_PROF_GEMM, gemm_f(fM, 3 * fC, fC), gemm_b(fM, 3 * fC, fC, 0), bt_gemm(BT_OP_N, BT_OP_N, M, 3 * C, C, ln1, C, P + w.Wqkv, 3 * C, 0.f, qkv, 3 * C, P + w.bqkv,
-                   BT_EPI_BIAS, nullptr, nullptr, nullptr, scr, scrb, s));
+                   BT_EPI_BIAS, nullptr, nullptr, nullptr, nullptr, scr, scrb, s));
     BT_PROF(BT_PROF_ATTN_FWD, attn_fwd_f, attn_fwd_b, bt_attention_fwd(qkv, att, sb.layer(ly.lse, l), B, T, H, hd, s));
     BT_PROF(BT_PROF_GEMM, gemm_f(fM, fC, fC), gemm_b(fM, fC, fC, 1), bt_gemm(BT_OP_N, BT_OP_N, M, C, C, att, C, P + w.Wo, C, 0.f, xmid, C, P + w.bo, BT_EPI_BIAS, nullptr,
-                   nullptr, sb.res(l), scr, scrb, s));
+                   nullptr, sb.res(l), nullptr, scr, scrb, s));
     BT_PROF(BT_PROF_LN_FWD, 0, ln_fwd_b, bt_layernorm_fwd(xmid, P + w.ln2g, P + w.ln2b, ln2, sb.layer(ly.mu2, l), sb.layer(ly.rs2, l), M, C,
                             cf.ln_eps, s));
     BT_PROF(BT_PROF_GEMM, gemm_f(fM, fF, fC), gemm_b(fM, fF, fC, 1), bt_gemm(BT_OP_N, BT_OP_N, M, F, C, ln2, C, P + w.Wfc, F, 0.f, gact, F, P + w.bfc, BT_EPI_BIAS_GELU, hpre,
-                   nullptr, nullptr, scr, scrb, s));
+                   nullptr, nullptr, nullptr, scr, scrb, s));
     BT_PROF(BT_PROF_GEMM, gemm_f(fM, fC, fF), gemm_b(fM, fC, fF, 1), bt_gemm(BT_OP_N, BT_OP_N, M, C, F, gact, F, P + w.Wfp, C, 0.f, sb.res(l + 1), C, P + w.bfp, BT_EPI_BIAS,
-                   nullptr, nullptr, xmid, scr, scrb, s));
+                   nullptr, nullptr, xmid, nullptr, scr, scrb, s));
   }
   float* lnf = sb.f(ly.lnf);
   float* logits = sb.f(ly.logits);
   float* lrows = sb.f(ly.loss_rows);
   BT_PROF(BT_PROF_LN_FWD, 0, ln_fwd_b, bt_layernorm_fwd(sb.res(L), P + po.lnfg, P + po.lnfb, lnf, sb.f(ly.muf), sb.f(ly.rsf), M, C, cf.ln_eps, s));
   BT_PROF(BT_PROF_GEMM, gemm_f(fM, fV, fC), gemm_b(fM, fV, fC, 0), bt_gemm(BT_OP_N, BT_OP_T, M, Vp, C, lnf, C, P + po.wte, C, 0.f, logits, Vp, nullptr, BT_EPI_NONE, nullptr,
-                 nullptr, nullptr, scr, scrb, s));
+                 nullptr, nullptr, nullptr, scr, scrb, s));
   // loss rows + dlogits = (softmax - onehot) * loss_scale, written over the logits
   BT_PROF(BT_PROF_XENT, 0, f4 * (2 * fM * fV + 3 * fM), bt_softmax_xent_fused(logits, targets, lrows, sb.f(ly.lse_rows), loss_scale, M, cf.V, Vp, s));
   BT_PROF(BT_PROF_OTHER, 0, f4 * fM, launch_loss_sum(lrows, M, loss_scale, accumulate, loss_dst, s));
@@ -425,9 +425,9 @@ extern "C" bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, floa
   float* dsm = sb.f(ly.dsmall);
   const float* dlogits = logits;
   BT_PROF(BT_PROF_GEMM, gemm_f(fM, fC, fV), gemm_b(fM, fC, fV, 0), bt_gemm(BT_OP_N, BT_OP_N, M, C, Vp, dlogits, Vp, P + po.wte, C, 0.f, dsm, C, nullptr, BT_EPI_NONE, nullptr,
-                 nullptr, nullptr, scr, scrb, s));  // dlnf
+                 nullptr, nullptr, nullptr, scr, scrb, s));  // dlnf
   BT_PROF(BT_PROF_GEMM, gemm_f(fV, fC, fM), gemm_b(fV, fC, fM, accumulate), bt_gemm(BT_OP_T, BT_OP_N, Vp, C, M, dlogits, Vp, lnf, C, beta, G + po.wte, C, nullptr, BT_EPI_NONE, nullptr,
-                 nullptr, nullptr, scr, scrb, s));  // dwte (LM head part)
+                 nullptr, nullptr, nullptr, scr, scrb, s));  // dwte (LM head part)
   BT_PROF(BT_PROF_LN_BWD, 0, ln_bwd_b0, bt_layernorm_bwd(dsm, sb.res(L), P + po.lnfg, sb.f(ly.muf), sb.f(ly.rsf), dres, G + po.lnfg, G + po.lnfb, 0.f,
                           beta, scr, scrb, M, C, s));
   for (int l = L - 1; l >= 0; --l) {
@@ -439,33 +439,30 @@ extern "C" bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, floa
     float* ln2 = sb.layer(ly.ln2, l);
     float* hpre = sb.layer(ly.h, l);
     float* gact = sb.layer(ly.g, l);
-    // MLP down-projection: dWfp += g^T dres ; dbfp += colsum(dres) ; dh = (dres Wfp^T) * gelu'(h)
+    // MLP down-projection: dWfp += g^T dres and dbfp += colsum(dres) in one product;
+    // dh = (dres Wfp^T) * gelu'(h)
     BT_PROF(BT_PROF_GEMM, gemm_f(fF, fC, fM), gemm_b(fF, fC, fM, accumulate), bt_gemm(BT_OP_T, BT_OP_N, F, C, M, gact, F, dres, C, beta, G + w.Wfp, C, nullptr, BT_EPI_NONE, nullptr,
-                   nullptr, nullptr, scr, scrb, s));
-    BT_PROF(BT_PROF_COLSUM, 0, f4 * fM * fC, bt_colsum(dres, M, C, C, G + w.bfp, beta, scr, scrb, s));
+                   nullptr, nullptr, G + w.bfp, scr, scrb, s));
     BT_PROF(BT_PROF_GEMM, gemm_f(fM, fF, fC), gemm_b(fM, fF, fC, 1), bt_gemm(BT_OP_N, BT_OP_T, M, F, C, dres, C, P + w.Wfp, C, 0.f, dbig, F, nullptr, BT_EPI_DGELU, nullptr,
-                   hpre, nullptr, scr, scrb, s));
-    // MLP up-projection: dWfc += ln2^T dh ; dbfc ; dln2 = dh Wfc^T
+                   hpre, nullptr, nullptr, scr, scrb, s));
+    // MLP up-projection: dWfc += ln2^T dh with dbfc ; dln2 = dh Wfc^T
     BT_PROF(BT_PROF_GEMM, gemm_f(fC, fF, fM), gemm_b(fC, fF, fM, accumulate), bt_gemm(BT_OP_T, BT_OP_N, C, F, M, ln2, C, dbig, F, beta, G + w.Wfc, F, nullptr, BT_EPI_NONE, nullptr,
-                   nullptr, nullptr, scr, scrb, s));
-    BT_PROF(BT_PROF_COLSUM, 0, f4 * fM * fF, bt_colsum(dbig, M, F, F, G + w.bfc, beta, scr, scrb, s));
+                   nullptr, nullptr, G + w.bfc, scr, scrb, s));
     BT_PROF(BT_PROF_GEMM, gemm_f(fM, fC, fF), gemm_b(fM, fC, fF, 0), bt_gemm(BT_OP_N, BT_OP_T, M, C, F, dbig, F, P + w.Wfc, F, 0.f, dsm, C, nullptr, BT_EPI_NONE, nullptr,
-                   nullptr, nullptr, scr, scrb, s));
+                   nullptr, nullptr, nullptr, scr, scrb, s));
     BT_PROF(BT_PROF_LN_BWD, 0, ln_bwd_b1, bt_layernorm_bwd(dsm, xmid, P + w.ln2g, sb.layer(ly.mu2, l), sb.layer(ly.rs2, l), dres, G + w.ln2g,
                             G + w.ln2b, 1.f, beta, scr, scrb, M, C, s));
-    // attention output projection: dWo += att^T dres ; dbo ; datt = dres Wo^T
+    // attention output projection: dWo += att^T dres with dbo ; datt = dres Wo^T
     BT_PROF(BT_PROF_GEMM, gemm_f(fC, fC, fM), gemm_b(fC, fC, fM, accumulate), bt_gemm(BT_OP_T, BT_OP_N, C, C, M, att, C, dres, C, beta, G + w.Wo, C, nullptr, BT_EPI_NONE, nullptr,
-                   nullptr, nullptr, scr, scrb, s));
-    BT_PROF(BT_PROF_COLSUM, 0, f4 * fM * fC, bt_colsum(dres, M, C, C, G + w.bo, beta, scr, scrb, s));
+                   nullptr, nullptr, G + w.bo, scr, scrb, s));
     BT_PROF(BT_PROF_GEMM, gemm_f(fM, fC, fC), gemm_b(fM, fC, fC, 0), bt_gemm(BT_OP_N, BT_OP_T, M, C, C, dres, C, P + w.Wo, C, 0.f, dsm, C, nullptr, BT_EPI_NONE, nullptr,
-                   nullptr, nullptr, scr, scrb, s));
+                   nullptr, nullptr, nullptr, scr, scrb, s));
     BT_PROF(BT_PROF_ATTN_BWD, attn_bwd_f, attn_bwd_b, bt_attention_bwd(dsm, qkv, att, sb.layer(ly.lse, l), dbig, scr, scrb, B, T, H, hd, s));
-    // QKV projection: dWqkv += ln1^T dqkv ; dbqkv ; dln1 = dqkv Wqkv^T
+    // QKV projection: dWqkv += ln1^T dqkv with dbqkv ; dln1 = dqkv Wqkv^T
     BT_PROF(BT_PROF_GEMM, gemm_f(fC, 3 * fC, fM), gemm_b(fC, 3 * fC, fM, accumulate), bt_gemm(BT_OP_T, BT_OP_N, C, 3 * C, M, ln1, C, dbig, 3 * C, beta, G + w.Wqkv, 3 * C, nullptr, BT_EPI_NONE,
-                   nullptr, nullptr, nullptr, scr, scrb, s));
-    BT_PROF(BT_PROF_COLSUM, 0, f4 * fM * 3 * fC, bt_colsum(dbig, M, 3 * C, 3 * C, G + w.bqkv, beta, scr, scrb, s));
+                   nullptr, nullptr, nullptr, G + w.bqkv, scr, scrb, s));
     BT_PROF(BT_PROF_GEMM, gemm_f(fM, fC, 3 * fC), gemm_b(fM, fC, 3 * fC, 0), bt_gemm(BT_OP_N, BT_OP_T, M, C, 3 * C, dbig, 3 * C, P + w.Wqkv, 3 * C, 0.f, dsm, C, nullptr, BT_EPI_NONE,
-                   nullptr, nullptr, nullptr, scr, scrb, s));
+                   nullptr, nullptr, nullptr, nullptr, scr, scrb, s));
     BT_PROF(BT_PROF_LN_BWD, 0, ln_bwd_b1, bt_layernorm_bwd(dsm, sb.res(l), P + w.ln1g, sb.layer(ly.mu1, l), sb.layer(ly.rs1, l), dres, G + w.ln1g,
                             G + w.ln1b, 1.f, beta, scr, scrb, M, C, s));
   }
@@ -476,7 +473,7 @@ extern "C" bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, floa
 }
 
 extern "C" bt_status bt_gpt2_optimizer_step(bt_gpt2_ctx* ctx, float* params, float* grads, float* opt_state, int t,
-                                            float lr) {
+                                            double lr) {
   BT_RETURN_IF(!ctx || !params || !grads || !opt_state, BT_EINVAL, "bt_gpt2_optimizer_step: NULL pointer");
   BT_RETURN_IF(t < 1, BT_EINVAL, "bt_gpt2_optimizer_step: t=%d must be >= 1", t);
   const bt_gpt2_config& cf = ctx->cfg;
@@ -485,9 +482,9 @@ extern "C" bt_status bt_gpt2_optimizer_step(bt_gpt2_ctx* ctx, float* params, flo
   float* d_scal = sb.f(ctx->lay.scalars);
   const float* coef = nullptr;
   BT_PROF(BT_PROF_GRAD_NORM, 2.0 * P, 4.0 * P,
-          bt_grad_norm_clip(grads, P, cf.grad_clip, d_scal + 1, d_scal + 2, sb.scratch(), sb.scratch_bytes(),
+          bt_grad_norm_clip(grads, P, (float)cf.grad_clip, d_scal + 1, d_scal + 2, sb.scratch(), sb.scratch_bytes(),
                             ctx->stream));
-  if (cf.grad_clip > 0.f) coef = d_scal + 2;
+  if (cf.grad_clip > 0.0) coef = d_scal + 2;
   BT_PROF(BT_PROF_ADAMW, 0, 28.0 * P,
           bt_adamw_step(params, grads, opt_state, opt_state + P, P, ctx->po.n_decay, lr, cf.beta1, cf.beta2,
                         cf.adam_eps, cf.weight_decay, t, coef, ctx->stream));

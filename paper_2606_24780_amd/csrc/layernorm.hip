@@ -4,9 +4,10 @@
 // One wave64 per row: the row (C <= 4096 floats) is held in registers as
 // float4, mean and variance come from two in-register passes reduced with
 // cross-lane shuffles (no LDS), so x is read once and y written once.  The
-// backward computes dx row-wise the same way; dgamma/dbeta are accumulated
-// per wave over a contiguous chunk of rows, combined per block through LDS
-// and written as block partials that a second kernel sums in a fixed order.
+// backward computes dx row-wise the same way (two rows per wave in flight);
+// dgamma/dbeta are accumulated per wave over a contiguous chunk of rows,
+// combined per block through LDS and written as one partial row per block
+// (at most 256 blocks), which a second kernel sums in a fixed order.
 #include "bt_internal.h"
 
 namespace bt {
@@ -68,18 +69,89 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ x
   }
 }
 
-// dx row-wise; per-block partial column sums of dy*xhat and dy.
+// Backward block: W waves (16 for rows up to 512 floats, fewer for wider
+// rows so the registers suffice); each wave takes rows r0+w, r0+w+W, ... of
+// the block's contiguous chunk, two rows at a time when they fit (both
+// rows' loads issued before either row's reductions).
 template <int NV>
-__global__ void __launch_bounds__(256) ln_bwd_kernel(const float* dy, const float* __restrict__ x,
-                                                     const float* __restrict__ gamma,
-                                                     const float* __restrict__ mean,
-                                                     const float* __restrict__ rstd, float* dx,
-                                                     float* __restrict__ part, int M, int C,
-                                                     int rows_per_block, float dx_beta) {
+struct BwdWaves {
+  static constexpr int value = NV <= 2 ? 16 : (NV <= 4 ? 8 : 4);
+};
+
+template <int NV>
+struct LnRow {
+  floatx4 d[NV], xh[NV];  // dy and xhat of the row (g = dy * gamma is recomputed)
+  float mg, mgx, rs;
+};
+
+template <int NV>
+__device__ __forceinline__ void ln_row_load(LnRow<NV>& r, const float* dy, const float* __restrict__ x,
+                                            const float* __restrict__ mean, const float* __restrict__ rstd,
+                                            const floatx4 (&gam)[NV], int row, int C4, int lane) {
+  const floatx4* dyr = reinterpret_cast<const floatx4*>(dy + (long long)row * 4 * C4);
+  const floatx4* xr = reinterpret_cast<const floatx4*>(x + (long long)row * 4 * C4);
+  const float mu = mean[row];
+  r.rs = rstd[row];
+  floatx4 xv[NV];
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = lane + 64 * i;
+    r.d[i] = c < C4 ? dyr[c] : floatx4{0.f, 0.f, 0.f, 0.f};
+    xv[i] = c < C4 ? xr[c] : floatx4{0.f, 0.f, 0.f, 0.f};
+  }
+  float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = lane + 64 * i;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      r.xh[i][k] = c < C4 ? (xv[i][k] - mu) * r.rs : 0.f;
+      const float g = r.d[i][k] * gam[i][k];
+      s1 += g;
+      s2 += g * r.xh[i][k];
+    }
+  }
+  r.mg = s1;
+  r.mgx = s2;
+}
+
+template <int NV>
+__device__ __forceinline__ void ln_row_store(const LnRow<NV>& r, const floatx4 (&gam)[NV], float* dx, int row, int C4,
+                                             int lane, float invC, float dx_beta, floatx4 (&acc_dg)[NV],
+                                             floatx4 (&acc_db)[NV]) {
+  const float mg = r.mg * invC, mgx = r.mgx * invC;
+  floatx4* dxr = reinterpret_cast<floatx4*>(dx + (long long)row * 4 * C4);
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const int c = lane + 64 * i;
+    if (c < C4) {
+      floatx4 o;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) o[k] = r.rs * (r.d[i][k] * gam[i][k] - mg - r.xh[i][k] * mgx);
+      if (dx_beta != 0.f) o += dxr[c];
+      dxr[c] = o;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        acc_dg[i][k] += r.d[i][k] * r.xh[i][k];
+        acc_db[i][k] += r.d[i][k];
+      }
+    }
+  }
+}
+
+// dx row-wise; per-block partial column sums of dy*xhat and dy.
+template <int NV, int BWD_WAVES = BwdWaves<NV>::value>
+__global__ void __launch_bounds__(64 * BWD_WAVES) ln_bwd_kernel(const float* dy, const float* __restrict__ x,
+                                                                const float* __restrict__ gamma,
+                                                                const float* __restrict__ mean,
+                                                                const float* __restrict__ rstd, float* dx,
+                                                                float* __restrict__ part, int M, int C,
+                                                                int rows_per_block, float dx_beta) {
   __shared__ floatx4 red[64 * NV][2];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int C4 = C >> 2;
+  const float invC = 1.0f / (float)C;
   const floatx4* g4 = reinterpret_cast<const floatx4*>(gamma);
   floatx4 gam[NV], acc_dg[NV], acc_db[NV];
 #pragma unroll
@@ -91,51 +163,29 @@ __global__ void __launch_bounds__(256) ln_bwd_kernel(const float* dy, const floa
   }
   const int r0 = blockIdx.x * rows_per_block;
   const int r1 = min(M, r0 + rows_per_block);
-  for (int row = r0 + wave; row < r1; row += ROWS_PER_BLOCK) {
-    const floatx4* dyr = reinterpret_cast<const floatx4*>(dy + (long long)row * C);
-    const floatx4* xr = reinterpret_cast<const floatx4*>(x + (long long)row * C);
-    const float mu = mean[row], rs = rstd[row];
-    floatx4 xh[NV], gg[NV], d[NV];
-    float s1 = 0.f, s2 = 0.f;
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int c = lane + 64 * i;
-      if (c < C4) {
-        d[i] = dyr[c];
-        const floatx4 xv = xr[c];
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          xh[i][k] = (xv[k] - mu) * rs;
-          gg[i][k] = d[i][k] * gam[i][k];
-          s1 += gg[i][k];
-          s2 += gg[i][k] * xh[i][k];
-        }
-      } else {
-        d[i] = xh[i] = gg[i] = floatx4{0.f, 0.f, 0.f, 0.f};
-      }
-    }
-    const float mg = wave_sum(s1) / (float)C;
-    const float mgx = wave_sum(s2) / (float)C;
-    floatx4* dxr = reinterpret_cast<floatx4*>(dx + (long long)row * C);
-#pragma unroll
-    for (int i = 0; i < NV; ++i) {
-      const int c = lane + 64 * i;
-      if (c < C4) {
-        floatx4 o;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) o[k] = rs * (gg[i][k] - mg - xh[i][k] * mgx);
-        if (dx_beta != 0.f) o += dxr[c];
-        dxr[c] = o;
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          acc_dg[i][k] += d[i][k] * xh[i][k];
-          acc_db[i][k] += d[i][k];
-        }
-      }
+  int row = r0 + wave;
+  if (NV <= 4) {
+    for (; row + BWD_WAVES < r1; row += 2 * BWD_WAVES) {
+      LnRow<NV> a, b;
+      ln_row_load<NV>(a, dy, x, mean, rstd, gam, row, C4, lane);
+      ln_row_load<NV>(b, dy, x, mean, rstd, gam, row + BWD_WAVES, C4, lane);
+      a.mg = wave_sum(a.mg);
+      b.mg = wave_sum(b.mg);
+      a.mgx = wave_sum(a.mgx);
+      b.mgx = wave_sum(b.mgx);
+      ln_row_store<NV>(a, gam, dx, row, C4, lane, invC, dx_beta, acc_dg, acc_db);
+      ln_row_store<NV>(b, gam, dx, row + BWD_WAVES, C4, lane, invC, dx_beta, acc_dg, acc_db);
     }
   }
-  // fixed-order combine of the 4 waves (wave 0 first), one partial row per block
-  for (int w = 0; w < ROWS_PER_BLOCK; ++w) {
+  for (; row < r1; row += BWD_WAVES) {
+    LnRow<NV> a;
+    ln_row_load<NV>(a, dy, x, mean, rstd, gam, row, C4, lane);
+    a.mg = wave_sum(a.mg);
+    a.mgx = wave_sum(a.mgx);
+    ln_row_store<NV>(a, gam, dx, row, C4, lane, invC, dx_beta, acc_dg, acc_db);
+  }
+  // fixed-order combine of the waves (wave 0 first), one partial row per block
+  for (int w = 0; w < BWD_WAVES; ++w) {
     if (wave == w) {
 #pragma unroll
       for (int i = 0; i < NV; ++i) {
@@ -152,29 +202,17 @@ __global__ void __launch_bounds__(256) ln_bwd_kernel(const float* dy, const floa
     __syncthreads();
   }
   floatx4* pg = reinterpret_cast<floatx4*>(part + (long long)blockIdx.x * 2 * C);
-  for (int c = threadIdx.x; c < C4; c += 256) {
+  for (int c = threadIdx.x; c < C4; c += 64 * BWD_WAVES) {
     pg[c] = red[c][0];
     pg[C4 + c] = red[c][1];
   }
 }
 
-__global__ void __launch_bounds__(256) ln_bwd_param_reduce(const float* __restrict__ part, int nblocks, int C,
-                                                           float* __restrict__ dgamma,
-                                                           float* __restrict__ dbeta, float beta) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= 2 * C) return;
-  float s = 0.f;
-  for (int b = 0; b < nblocks; ++b) s += part[(long long)b * 2 * C + c];
-  float* dst = c < C ? dgamma + c : dbeta + (c - C);
-  if (beta != 0.f) s += *dst;
-  *dst = s;
-}
-
 int ln_nv(int C) { return (C / 4 + 63) / 64; }
 
 int ln_bwd_blocks(int M) {
-  int nb = (M + 31) / 32;  // >= 32 rows per block (8 per wave)
-  if (nb > 1024) nb = 1024;
+  int nb = (M + 63) / 64;  // >= 64 rows per 16-wave block
+  if (nb > 256) nb = 256;  // one block per CU: few partials to combine
   if (nb < 1) nb = 1;
   return nb;
 }
@@ -249,11 +287,9 @@ extern "C" bt_status bt_layernorm_bwd(const float* dy, const float* x, const flo
   const int nb = ln_bwd_blocks(M);
   const int rpb = (M + nb - 1) / nb;
   float* part = static_cast<float*>(ws);
-#define BT_LN_BWD(NV) hipLaunchKernelGGL(ln_bwd_kernel<NV>, dim3(nb), dim3(256), 0, s, dy, x, gamma, mean, rstd, dx, part, M, C, rpb, dx_beta)
+#define BT_LN_BWD(NV) hipLaunchKernelGGL(ln_bwd_kernel<NV>, dim3(nb), dim3(64 * BwdWaves<NV>::value), 0, s, dy, x, gamma, mean, rstd, dx, part, M, C, rpb, dx_beta)
   BT_LN_DISPATCH(ln_nv(C), BT_LN_BWD)
 #undef BT_LN_BWD
   BT_TRY(check_launch("ln_bwd_kernel"));
-  hipLaunchKernelGGL(ln_bwd_param_reduce, dim3((2 * C + 255) / 256), dim3(256), 0, s, part, nb, C, dgamma, dbeta,
-                     param_beta);
-  return check_launch("ln_bwd_param_reduce");
+  return sum_partials(part, nb, 2LL * C, 2 * C, dgamma, C, dbeta, param_beta, s);
 }

@@ -34,9 +34,13 @@ __global__ void __launch_bounds__(XT) xent_row_kernel(float* logits, const int32
                                                       float* __restrict__ loss_rows, float* __restrict__ lse_out,
                                                       float* dlogits, float scale, int V, int Vp) {
   __shared__ float red[XT / 64];
+  __shared__ float s_zy;
   const int row = blockIdx.x;
   const int tid = threadIdx.x;
   const int V4 = Vp >> 2;
+  int y = targets[row];
+  const bool bad = y < 0 || y >= V;
+  if (bad) y = 0;
   const floatx4* zr = reinterpret_cast<const floatx4*>(logits + (long long)row * Vp);
   floatx4 z[NPT];
   float mx = -INFINITY;
@@ -47,14 +51,13 @@ __global__ void __launch_bounds__(XT) xent_row_kernel(float* logits, const int32
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       if (4 * c4 + k >= V) z[i][k] = -INFINITY;  // padded columns are outside the softmax
+      if (4 * c4 + k == y) s_zy = z[i][k];       // the target logit, taken from registers: the
+                                                 // row is overwritten in place below
       mx = fmaxf(mx, z[i][k]);
     }
   }
-  mx = block_reduce(mx, red, true);
-  int y = targets[row];
-  const bool bad = y < 0 || y >= V;
-  if (bad) y = 0;
-  const float zy = logits[(long long)row * Vp + y];
+  mx = block_reduce(mx, red, true);  // its barriers also publish s_zy
+  const float zy = s_zy;
   const float mxl = mx * LOG2E_X;
   float s = 0.f;
 #pragma unroll

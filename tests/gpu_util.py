@@ -40,10 +40,14 @@ def err_report(got, ref):
                 inf=float(np.abs(d).max()), scale=scale)
 
 
-def assert_close_maxabs(got, ref, tol, what=""):
+def assert_close_maxabs(got, ref, tol, what="", scale=None):
     """|got - ref| <= tol * max|ref| element-wise (the bar used for every
-    floating-point tensor)."""
+    floating-point tensor).  `scale` overrides max|ref| where the reference
+    is identically zero in exact arithmetic (then its natural magnitude is
+    the scale of the inputs that cancel)."""
     r = err_report(got, ref)
+    if scale is not None:
+        r["maxabs_rel"] = r["inf"] / scale
     print(f"[parity] {what}: maxabs_rel={r['maxabs_rel']:.3e} l2_rel={r['l2_rel']:.3e}", file=sys.stderr)
     assert np.isfinite(np.asarray(got)).all(), f"{what}: non-finite values"
     assert r["maxabs_rel"] <= tol, f"{what}: max-abs-relative error {r['maxabs_rel']:.3e} > {tol:.1e}"

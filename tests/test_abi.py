@@ -62,8 +62,9 @@ def test_status_strings(lib):
 
 
 def _gemm(lib, opA=0, opB=0, M=128, N=128, K=128, A=FAKE, lda=128, B=FAKE, ldb=128, beta=0.0, C=FAKE,
-          ldc=128, bias=None, epi=0, pre=None, gin=None, res=None, ws=None, wsb=0):
-    return lib.bt_gemm(opA, opB, M, N, K, A, lda, B, ldb, beta, C, ldc, bias, epi, pre, gin, res, ws, wsb, None)
+          ldc=128, bias=None, epi=0, pre=None, gin=None, res=None, cs=None, ws=None, wsb=0):
+    return lib.bt_gemm(opA, opB, M, N, K, A, lda, B, ldb, beta, C, ldc, bias, epi, pre, gin, res, cs, ws, wsb,
+                       None)
 
 
 def test_gemm_validation(lib):
@@ -76,6 +77,8 @@ def test_gemm_validation(lib):
     assert _gemm(lib, res=FAKE) == BT_EINVAL        # residual aliases C
     assert _gemm(lib, opA=5) == BT_EINVAL
     assert _gemm(lib, C=None) == BT_EINVAL
+    assert _gemm(lib, opB=1, cs=FAKE + 4096) == BT_EINVAL   # column sums need op(B) = B
+    assert _gemm(lib, epi=1, bias=FAKE, cs=FAKE + 4096) == BT_EINVAL
     assert b"multiples of 4" in lib.bt_last_error() or True
     # a split-K shape without workspace
     need = lib.bt_gemm_ws_bytes(1, 0, 768, 768, 16384, 0)

@@ -39,8 +39,11 @@ def test_attention_small(B, T, H, hd):
     r_dqkv = ops.attention_bwd(dout, qkv, H)
     assert_close_maxabs(out, r_out, 1e-5, "out")
     assert_close_maxabs(lse, r_lse, 1e-5, "lse")
+    # dqkv is one gradient tensor: bar relative to its max-abs (with T = 1 the
+    # dQ and dK blocks are exactly zero and only rounding remains)
+    assert_close_maxabs(dqkv, r_dqkv, 1e-4, "dqkv")
     for i, n in enumerate("QKV"):
-        assert_close_maxabs(dqkv[:, :, i], r_dqkv[:, :, i], 1e-4, f"d{n}")
+        assert_close_maxabs(dqkv[:, :, i], r_dqkv[:, :, i], 1e-4, f"d{n}", scale=np.abs(r_dqkv).max())
 
 
 def test_attention_q_zero_closed_form():

@@ -117,3 +117,21 @@ def test_gemm_gpt2_124m_shapes_sampled(K, N):
     bt.bt_gemm(1, 0, K, N, M, X, K, dY, N, 0.0, dW, N)
     dYc = host(dY[:, torch.from_numpy(cols).cuda()])
     assert_close_maxabs(host(dW)[:, cols], host(X).T @ dYc, TOL, f"TN {K}x{N}x{M}")
+
+
+@pytest.mark.parametrize("M,N,K", [(768, 768, 16384), (64, 192, 256), (260, 196, 132), (3072, 768, 4096)])
+def test_gemm_weight_grad_with_bias_grad(M, N, K):
+    """dW = X^T dY (TN) with the bias gradient sum_m dY[m, n] returned by the
+    same product (split-K and single-pass shapes), overwrite and accumulate."""
+    torch = torch_gpu()
+    say(f"gemm TN + column sums M={M} N={N} K={K}")
+    X = RNG.standard_normal((K, M)).astype(np.float32)
+    dY = RNG.standard_normal((K, N)).astype(np.float32)
+    C0 = RNG.standard_normal((M, N)).astype(np.float32)
+    cs0 = RNG.standard_normal(N).astype(np.float32)
+    for beta in (0.0, 1.0):
+        C = dev(torch, C0)
+        cs = dev(torch, cs0)
+        bt.bt_gemm(1, 0, M, N, K, dev(torch, X), M, dev(torch, dY), N, beta, C, N, colsum_B=cs)
+        assert_close_maxabs(host(C), ops.gemm(X, dY, True) + beta * C0, TOL, f"dW beta={beta}")
+        assert_close_maxabs(host(cs), dY.astype(np.float64).sum(0) + beta * cs0, TOL, f"db beta={beta}")

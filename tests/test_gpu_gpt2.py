@@ -60,16 +60,19 @@ def _check_update(cfg, hp, specs, params0, g_gpu, p_gpu, m_gpu, v_gpu, t, coef_g
     return norm, coef
 
 
-def _check_end_to_end(hp, specs, params0, g_gpu, g_or, p_gpu, p_or):
+def _check_end_to_end(hp, specs, params0, g_gpu, g_or, p_gpu, p_or, c_gpu=1.0, c_or=1.0):
     """End-to-end params: elementwise within 1e-5 max-abs, or within the
-    t = 1 sensitivity lr * eps * |dg| / (min|g| + eps)^2 of the update."""
+    t = 1 sensitivity of the update u(x) = x / (|x| + eps) of the clipped
+    gradient x = c g: lr * eps * |x_gpu - x_or| / (min|x| + eps)^2 (mean-value
+    bound on an interval of one sign)."""
     worst = 0.0
     for name, _, _ in specs:
         d = np.abs(p_gpu[name] - p_or[name])
         scale = np.abs(p_or[name]).max()
-        gmin = np.minimum(np.abs(g_gpu[name]), np.abs(g_or[name]))
-        bound = hp.lr * hp.eps * np.abs(g_gpu[name] - g_or[name]) / (gmin + hp.eps) ** 2 + PARAM_TOL * scale
-        same_sign = np.sign(g_gpu[name]) == np.sign(g_or[name])
+        xg, xo = c_gpu * g_gpu[name], c_or * g_or[name]
+        xmin = np.minimum(np.abs(xg), np.abs(xo))
+        bound = hp.lr * hp.eps * np.abs(xg - xo) / (xmin + hp.eps) ** 2 + PARAM_TOL * scale
+        same_sign = np.sign(xg) == np.sign(xo)
         bound = np.where(same_sign, bound, 2 * hp.lr + PARAM_TOL * scale)
         assert (d <= bound * (1 + 1e-6) + 1e-12).all(), f"end-to-end {name}"
         worst = max(worst, float(d.max() / scale))
@@ -228,4 +231,4 @@ def test_gpt2_124m_replicated_sequence_full_step():
         assert_close_maxabs(g[name], ref["grads"][name], GRAD_TOL, f"grad {name}")
     norm, coef = _check_update(cfg, hp, specs, params, g, p, m, v, 1, what="124M")
     assert abs(coef - coef_gpu) <= 1e-6 * coef
-    _check_end_to_end(hp, specs, params, g, ref["grads"], p, ref["params"])
+    _check_end_to_end(hp, specs, params, g, ref["grads"], p, ref["params"], coef_gpu, ref["coef"])

@@ -60,10 +60,10 @@ def test_gelu(n):
     xd = dev(torch, x)
     y = torch.empty_like(xd)
     bt.bt_gelu_fwd(xd, y)
-    assert_close_maxabs(host(y), ops.gelu_fwd(x), 1e-6, "gelu")
+    assert_close_maxabs(host(y), ops.gelu_fwd(x), 1e-5, "gelu")
     dyd = dev(torch, dy)
     bt.bt_gelu_bwd(xd, dyd, dyd)  # in place over dy
-    assert_close_maxabs(host(dyd), ops.gelu_bwd(x, dy), 1e-6, "gelu bwd (in place)")
+    assert_close_maxabs(host(dyd), ops.gelu_bwd(x, dy), 1e-5, "gelu bwd (in place)")
 
 
 # --------------------------------------------------------------- Cross-entropy
@@ -85,13 +85,14 @@ def test_xent(M, V, Vp):
     rdz = ops.xent_bwd(z, y, V, scale)
     dz = torch.empty_like(zd)
     bt.bt_softmax_xent_bwd(zd, lse, yd, dz, scale, M, V, Vp)
-    assert_close_maxabs(host(dz), rdz, 1e-5, "dlogits (bwd)")
+    # the natural scale of dlogits is `scale` (with V = 1 the gradient is exactly 0)
+    assert_close_maxabs(host(dz), rdz, 1e-5, "dlogits (bwd)", scale=max(np.abs(rdz).max(), scale))
     assert np.all(host(dz)[:, V:] == 0)
     loss2 = torch.empty(M, device="cuda")
     lse2 = torch.empty(M, device="cuda")
     bt.bt_softmax_xent_fused(zd, yd, loss2, lse2, scale, M, V, Vp)  # in place
     assert np.allclose(host(loss2), rl, rtol=1e-5, atol=1e-5 * max(1.0, np.abs(rl).max()))
-    assert_close_maxabs(host(zd), rdz, 1e-5, "dlogits (fused, in place)")
+    assert_close_maxabs(host(zd), rdz, 1e-5, "dlogits (fused, in place)", scale=max(np.abs(rdz).max(), scale))
     assert np.all(host(zd)[:, V:] == 0)
     # rows of (softmax - onehot) sum to zero
     assert np.abs(host(zd)[:, :V].sum(axis=1)).max() <= 1e-6 * scale * 10
