@@ -41,6 +41,7 @@ constexpr int BM = 128, BN = 128;
 constexpr int LDM = BM + 4;   // row stride of MN-contiguous LDS tiles (BM == BN)
 constexpr int NTHREADS = 256;
 constexpr int NUM_CU = 256;
+constexpr size_t MAX_SPLIT_WS = (size_t)1 << 30;  // largest split-K partial buffer considered
 
 struct GemmParams {
   const float* A;
@@ -347,11 +348,12 @@ GemmCfg choose_config(int M, int N, int K, bool akc, bool bkc, bool may_split) {
     const int occ = occupancy_for(bk, akc, bkc);
     const int kt = (K + bk - 1) / bk;
     int smax = 1;
-    if (may_split && tiles < 2LL * NUM_CU * occ && K >= 8 * bk) smax = kt / 4 < 32 ? kt / 4 : 32;
+    if (may_split && K >= 8 * bk) smax = kt / 4 < 32 ? kt / 4 : 32;
     for (int s = 1; s <= smax; ++s) {
       int ks = (K + s - 1) / s;
       ks = (ks + bk - 1) / bk * bk;
       if ((K + ks - 1) / ks != s) continue;
+      if (s > 1 && (double)s * M * N * sizeof(float) > (double)MAX_SPLIT_WS) continue;
       // time in 128 x 128 x 16 tile steps.  Measured on MI355X: with a
       // K-contiguous operand, BK = 16 at 3-4 resident blocks runs each step
       // about 5% faster than BK = 32 at 2 (more waves hide the barriers);

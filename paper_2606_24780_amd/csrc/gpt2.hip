@@ -99,20 +99,21 @@ size_t scratch_need(const bt_gpt2_config& c, int B, int T) {
   const int M = B * T, C = c.C, F = 4 * c.C;
   size_t s = 0;
   auto mx = [&](size_t v) { s = v > s ? v : s; };
-  // every product of the step without an epilogue may be split along K
-  mx(bt_gemm_ws_bytes(BT_OP_T, BT_OP_N, C, 3 * C, M, BT_EPI_NONE));
-  mx(bt_gemm_ws_bytes(BT_OP_T, BT_OP_N, C, C, M, BT_EPI_NONE));
-  mx(bt_gemm_ws_bytes(BT_OP_T, BT_OP_N, C, F, M, BT_EPI_NONE));
-  mx(bt_gemm_ws_bytes(BT_OP_T, BT_OP_N, F, C, M, BT_EPI_NONE));
-  mx(bt_gemm_ws_bytes(BT_OP_T, BT_OP_N, c.Vp, C, M, BT_EPI_NONE));
-  mx(bt_gemm_ws_bytes(BT_OP_N, BT_OP_N, M, C, c.Vp, BT_EPI_NONE));
-  mx(bt_gemm_ws_bytes(BT_OP_N, BT_OP_T, M, c.Vp, C, BT_EPI_NONE));
-  mx(bt_gemm_ws_bytes(BT_OP_N, BT_OP_T, M, C, 3 * C, BT_EPI_NONE));
-  mx(bt_gemm_ws_bytes(BT_OP_N, BT_OP_T, M, C, C, BT_EPI_NONE));
-  mx(bt_gemm_ws_bytes(BT_OP_N, BT_OP_T, M, C, F, BT_EPI_NONE));
-  // a split product never needs more than (512 + tiles) tiles of 128 x 128
-  // partials with tiles < 512, whatever the token count of the call
-  mx((size_t)1024 * 128 * 128 * sizeof(float) + (size_t)64 * (F > 3 * C ? F : 3 * C) * sizeof(float));
+  // every product of the step without an epilogue may be split along K; the
+  // split count depends on the token count, so cover every call size <= M
+  for (int m = M; m >= 1; m = m > 1 ? (m + 1) / 2 : 0) {
+    mx(bt_gemm_ws_bytes(BT_OP_T, BT_OP_N, C, 3 * C, m, BT_EPI_NONE));
+    mx(bt_gemm_ws_bytes(BT_OP_T, BT_OP_N, C, C, m, BT_EPI_NONE));
+    mx(bt_gemm_ws_bytes(BT_OP_T, BT_OP_N, C, F, m, BT_EPI_NONE));
+    mx(bt_gemm_ws_bytes(BT_OP_T, BT_OP_N, F, C, m, BT_EPI_NONE));
+    mx(bt_gemm_ws_bytes(BT_OP_T, BT_OP_N, c.Vp, C, m, BT_EPI_NONE));
+    mx(bt_gemm_ws_bytes(BT_OP_N, BT_OP_N, m, C, c.Vp, BT_EPI_NONE));
+    mx(bt_gemm_ws_bytes(BT_OP_N, BT_OP_T, m, c.Vp, C, BT_EPI_NONE));
+    mx(bt_gemm_ws_bytes(BT_OP_N, BT_OP_T, m, C, 3 * C, BT_EPI_NONE));
+    mx(bt_gemm_ws_bytes(BT_OP_N, BT_OP_T, m, C, C, BT_EPI_NONE));
+    mx(bt_gemm_ws_bytes(BT_OP_N, BT_OP_T, m, C, F, BT_EPI_NONE));
+    if (m == 1) break;
+  }
   mx(bt_attention_bwd_ws_bytes(B, T, c.H, C / c.H));
   mx(bt_layernorm_bwd_ws_bytes(M, C));
   mx(bt_colsum_ws_bytes(M, F > 3 * C ? F : 3 * C));
