@@ -36,7 +36,40 @@ def parse():
     ap.add_argument("--seq", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=2048)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run 3 plain device copies of 1 GiB (reference for HBM byte counters)")
     return ap.parse_args()
+
+
+def gemm_traffic():
+    """HBM bytes per GEMM launch from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE passes (scaled by a plain 1 GiB copy), or None when the GEMM
+    source has changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "gemm_f32_mfma_gpt2_124m_b16_traffic.json")
+    src = os.path.join(ROOT, "paper_2606_24780_amd", "csrc", "gemm.hip")
+    try:
+        rec = json.load(open(path))
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+    except (OSError, ValueError):
+        return None, None
+    if rec.get("gemm_source_sha256") != sha:
+        return None, rec.get("algorithmic_bytes_per_launch")
+    return rec.get("traffic_bytes_per_launch"), rec.get("algorithmic_bytes_per_launch")
+
+
+def calibrate_copy():
+    """A plain copy kernel of known size: the per-dispatch FETCH_SIZE and
+    WRITE_SIZE counters it produces scale the counters of the path's kernels
+    to bytes."""
+    import torch
+    n = (1 << 30) // 4
+    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "dispatches": 3}))
 
 
 def cpu_baseline(sample_tokens: int):
@@ -69,6 +102,9 @@ def cpu_baseline(sample_tokens: int):
 
 def main():
     a = parse()
+    if a.calibrate_copy:
+        calibrate_copy()
+        return
     if a.gpus != 1:
         print(f"bench.py: only --gpus 1 is supported by this build (got {a.gpus}); "
               "the multi-GPU data-parallel exchange is not implemented", file=sys.stderr)
@@ -129,10 +165,13 @@ def main():
             k["gbs"] = st["bytes"] / (st["ms"] / 1e3) / 1e9
             k["frac_hbm"] = k["gbs"] / HBM_PEAK_GBS
         kernels[name] = k
+    traffic, algo_bytes = gemm_traffic()
     roofline = {
         "kernel": "gemm_f32_mfma (all bt_gemm calls of the step, incl. split-K reduction)",
         "bound": "mfma", "achieved": round(gemm_tflops, 3), "peak": MFMA_FP32_PEAK_TFLOPS,
-        "unit": "TFLOP/s", "frac": round(gemm_tflops / MFMA_FP32_PEAK_TFLOPS, 4), "traffic": None,
+        "unit": "TFLOP/s", "frac": round(gemm_tflops / MFMA_FP32_PEAK_TFLOPS, 4), "traffic": traffic,
+        "traffic_unit": "bytes per launch (L2-to-memory FETCH_SIZE + WRITE_SIZE, copy-scaled)",
+        "algorithmic_bytes_per_launch": algo_bytes,
         "launches": g["launches"], "avg_launch_ms": g["ms"] / max(1, g["launches"]),
         "flops_per_launch": g["flops"] / max(1, g["launches"]),
     }

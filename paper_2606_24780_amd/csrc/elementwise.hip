@@ -46,26 +46,46 @@ struct AdamArgs {
   float inv_bc1, inv_bc2;  // 1/(1-beta1^t), 1/(1-beta2^t)
 };
 
+__device__ __forceinline__ void adamw_vec(floatx4& pp, const floatx4& gg, floatx4& mm, floatx4& vv, float dec, float c,
+                                          const AdamArgs& a) {
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const float gk = gg[k] * c;
+    mm[k] = a.beta1 * mm[k] + a.omb1 * gk;
+    vv[k] = a.beta2 * vv[k] + a.omb2 * (gk * gk);
+    const float mhat = mm[k] * a.inv_bc1;
+    const float vhat = vv[k] * a.inv_bc2;
+    pp[k] = pp[k] - dec * pp[k] - a.lr * mhat / (sqrtf(vhat) + a.eps);
+  }
+}
+
+// Two float4 of each of p, g, m, v in flight per thread per iteration.
 __global__ void __launch_bounds__(EW_THREADS) adamw_kernel(floatx4* __restrict__ p, const floatx4* __restrict__ g,
                                                            floatx4* __restrict__ m, floatx4* __restrict__ v,
                                                            size_t n4, size_t nd4, AdamArgs a,
                                                            const float* __restrict__ grad_scale) {
   const float c = grad_scale ? *grad_scale : 1.f;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (size_t)gridDim.x * blockDim.x) {
-    floatx4 pp = p[i], gg = g[i], mm = m[i], vv = v[i];
-    const float dec = i < nd4 ? a.lr_wd : 0.f;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const float gk = gg[k] * c;
-      mm[k] = a.beta1 * mm[k] + a.omb1 * gk;
-      vv[k] = a.beta2 * vv[k] + a.omb2 * (gk * gk);
-      const float mhat = mm[k] * a.inv_bc1;
-      const float vhat = vv[k] * a.inv_bc2;
-      pp[k] = pp[k] - dec * pp[k] - a.lr * mhat / (sqrtf(vhat) + a.eps);
-    }
-    p[i] = pp;
-    m[i] = mm;
-    v[i] = vv;
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (; i + stride < n4; i += 2 * stride) {
+    const size_t i1 = i + stride;
+    floatx4 p0 = p[i], g0 = g[i], m0 = m[i], v0 = v[i];
+    floatx4 p1 = p[i1], g1 = g[i1], m1 = m[i1], v1 = v[i1];
+    adamw_vec(p0, g0, m0, v0, i < nd4 ? a.lr_wd : 0.f, c, a);
+    adamw_vec(p1, g1, m1, v1, i1 < nd4 ? a.lr_wd : 0.f, c, a);
+    p[i] = p0;
+    m[i] = m0;
+    v[i] = v0;
+    p[i1] = p1;
+    m[i1] = m1;
+    v[i1] = v1;
+  }
+  if (i < n4) {
+    floatx4 p0 = p[i], g0 = g[i], m0 = m[i], v0 = v[i];
+    adamw_vec(p0, g0, m0, v0, i < nd4 ? a.lr_wd : 0.f, c, a);
+    p[i] = p0;
+    m[i] = m0;
+    v[i] = v0;
   }
 }
 
@@ -73,11 +93,19 @@ __global__ void __launch_bounds__(EW_THREADS) adamw_kernel(floatx4* __restrict__
 __global__ void __launch_bounds__(EW_THREADS) sumsq_kernel(const floatx4* __restrict__ g, size_t n4,
                                                            double* __restrict__ part) {
   __shared__ double red[EW_THREADS / 64];
-  double s = 0.0;
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (size_t)gridDim.x * blockDim.x) {
+  double s = 0.0, s1 = 0.0;
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (; i + stride < n4; i += 2 * stride) {  // two loads in flight per thread
+    const floatx4 v = g[i], w = g[i + stride];
+    s += (double)v[0] * v[0] + (double)v[1] * v[1] + (double)v[2] * v[2] + (double)v[3] * v[3];
+    s1 += (double)w[0] * w[0] + (double)w[1] * w[1] + (double)w[2] * w[2] + (double)w[3] * w[3];
+  }
+  if (i < n4) {
     const floatx4 v = g[i];
     s += (double)v[0] * v[0] + (double)v[1] * v[1] + (double)v[2] * v[2] + (double)v[3] * v[3];
   }
+  s += s1;
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) s += __shfl_xor(s, o, 64);
   if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = s;

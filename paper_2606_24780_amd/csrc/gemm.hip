@@ -128,22 +128,52 @@ __device__ __forceinline__ floatx4 read_frag(const float* __restrict__ s, int ro
   }
 }
 
+// Epilogue of one 32 x 32 accumulator block (register r of lane (lr, hh) is
+// row i0 + 8 (r/4) + 4 hh + r%4, column j).  Every input the epilogue reads
+// (bias, GELU pre-activation, residual, old C) is loaded before the first
+// store: C may alias nothing, but the compiler cannot know that, and
+// interleaved load/store pairs would serialise on memory latency.
 template <int EPI>
-__device__ __forceinline__ void epilogue_store(const GemmParams& p, int i, int j, float acc) {
-  const long long off = (long long)i * p.ldc + j;
-  float v = acc;
-  if (EPI == BT_EPI_BIAS) {
-    v += p.bias[j];
-  } else if (EPI == BT_EPI_BIAS_GELU) {
-    const float pre = v + p.bias[j];
-    if (p.preact) p.preact[off] = pre;
-    v = gelu_f(pre);
-  } else if (EPI == BT_EPI_DGELU) {
-    v *= gelu_grad_f(p.gelu_in[off]);
+__device__ __forceinline__ void epilogue_block(const GemmParams& p, const floatx16& acc, int i0, int j, int hh) {
+  if (j >= p.N) return;
+  const bool has_res = p.residual != nullptr;
+  const bool has_old = p.beta != 0.f;
+  float bj = 0.f;
+  if (EPI == BT_EPI_BIAS || EPI == BT_EPI_BIAS_GELU) bj = p.bias[j];
+  constexpr int EC = 4;  // rows whose inputs are loaded together
+#pragma unroll
+  for (int r0 = 0; r0 < 16; r0 += EC) {
+    float gin[EC], res[EC], old[EC];
+#pragma unroll
+    for (int e = 0; e < EC; ++e) {
+      const int r = r0 + e;
+      const int i = i0 + 8 * (r >> 2) + 4 * hh + (r & 3);
+      const bool ok = i < p.M;
+      const long long off = (long long)i * p.ldc + j;
+      gin[e] = (EPI == BT_EPI_DGELU && ok) ? p.gelu_in[off] : 0.f;
+      res[e] = (has_res && ok) ? p.residual[off] : 0.f;
+      old[e] = (has_old && ok) ? p.C[off] : 0.f;
+    }
+#pragma unroll
+    for (int e = 0; e < EC; ++e) {
+      const int r = r0 + e;
+      const int i = i0 + 8 * (r >> 2) + 4 * hh + (r & 3);
+      if (i >= p.M) continue;
+      const long long off = (long long)i * p.ldc + j;
+      float v = acc[r];
+      if (EPI == BT_EPI_BIAS) {
+        v += bj;
+      } else if (EPI == BT_EPI_BIAS_GELU) {
+        const float pre = v + bj;
+        if (p.preact) p.preact[off] = pre;
+        v = gelu_f(pre);
+      } else if (EPI == BT_EPI_DGELU) {
+        v *= gelu_grad_f(gin[e]);
+      }
+      v += res[e] + old[e];
+      p.C[off] = v;
+    }
   }
-  if (p.residual) v += p.residual[off];
-  if (p.beta != 0.f) v += p.C[off];
-  p.C[off] = v;
 }
 
 template <bool A_KC, bool B_KC, int EPI, bool SPLIT, bool COLSUM, int BK, int OCC>
@@ -272,15 +302,16 @@ __global__ void __launch_bounds__(NTHREADS, OCC) gemm_f32_mfma(const GemmParams 
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb) {
       const int j = n0 + wn * 64 + nb * 32 + lr;
-      if (j >= p.N) continue;
+      const int i0 = m0 + wm * 64 + mb * 32;
+      if (SPLIT) {
+        if (j >= p.N) continue;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int i = m0 + wm * 64 + mb * 32 + 8 * (r >> 2) + 4 * hh + (r & 3);
-        if (i >= p.M) continue;
-        if (SPLIT)
-          p.ws[(long long)z * p.M * p.N + (long long)i * p.N + j] = acc[mb][nb][r];
-        else
-          epilogue_store<EPI>(p, i, j, acc[mb][nb][r]);
+        for (int r = 0; r < 16; ++r) {
+          const int i = i0 + 8 * (r >> 2) + 4 * hh + (r & 3);
+          if (i < p.M) p.ws[(long long)z * p.M * p.N + (long long)i * p.N + j] = acc[mb][nb][r];
+        }
+      } else {
+        epilogue_block<EPI>(p, acc[mb][nb], i0, j, hh);
       }
     }
 }

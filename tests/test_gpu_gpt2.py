@@ -232,3 +232,55 @@ def test_gpt2_124m_replicated_sequence_full_step():
     norm, coef = _check_update(cfg, hp, specs, params, g, p, m, v, 1, what="124M")
     assert abs(coef - coef_gpu) <= 1e-6 * coef
     _check_end_to_end(hp, specs, params, g, ref["grads"], p, ref["params"], coef_gpu, ref["coef"])
+
+
+@pytest.mark.timeout(900)
+def test_gpt2_124m_b64_equals_4x16_accumulation():
+    """Large-batch path: one step at B=64 against 4 micro-steps of 16 rows
+    with gradient accumulation (same tokens); gradients to the gradient bar,
+    each update to the oracle's AdamW of its own gradients, and the two
+    updates to each other within the t = 1 sensitivity of AdamW.  Also the
+    per-position losses of one sequence of the big batch against the oracle."""
+    torch = torch_gpu()
+    cfg = synth.GPT2_124M
+    hp = synth.HP_124M
+    specs = synth.param_specs(cfg)
+    params = synth.init_params(cfg, 4)
+    stream = synth.zipf_tokens(64 * 1024 + 1, cfg.V, 1.1, 50)
+    x, y = synth.shifted_pair(stream, 64, 1024)
+    say("gpt2 124M B=64 step")
+    torch.cuda.reset_peak_memory_stats()
+    big = bt.GPT2(cfg, hp, 64, 1024)
+    big.load_params(synth.flatten(cfg, params))
+    rows = torch.zeros(64 * 1024, device="cuda")
+    d_loss = torch.zeros(1, device="cuda")
+    big.fwd_bwd(dev(torch, x), dev(torch, y), 1.0 / (64 * 1024), 0, d_loss, rows)
+    big.optimizer_step(1, hp.lr)
+    torch.cuda.synchronize()
+    say(f"peak device memory at B=64: {torch.cuda.max_memory_allocated() / 2**30:.2f} GiB")
+    g64 = _unflat(cfg, big.grads)
+    p64, m64, v64 = _unflat(cfg, big.params), _unflat(cfg, big.m), _unflat(cfg, big.v)
+    rows64 = host(rows).reshape(64, 1024)
+    loss64 = float(d_loss.item())
+    del big
+    torch.cuda.empty_cache()
+    say("gpt2 124M 4 x 16 accumulation")
+    acc = bt.GPT2(cfg, hp, 16, 1024)
+    acc.load_params(synth.flatten(cfg, params))
+    d_loss2 = torch.zeros(1, device="cuda")
+    for k in range(4):
+        acc.fwd_bwd(dev(torch, x[16 * k:16 * k + 16]), dev(torch, y[16 * k:16 * k + 16]), 1.0 / (64 * 1024),
+                    k > 0, d_loss2)
+    acc.optimizer_step(1, hp.lr)
+    torch.cuda.synchronize()
+    assert abs(float(d_loss2.item()) - loss64) <= 1e-5 * loss64
+    ga = _unflat(cfg, acc.grads)
+    for name, _, _ in specs:
+        assert_close_maxabs(ga[name], g64[name], GRAD_TOL, f"4x16 vs 64 grad {name}")
+    _, c64 = _check_update(cfg, hp, specs, params, g64, p64, m64, v64, 1, what="B=64")
+    _, cacc = _check_update(cfg, hp, specs, params, ga, _unflat(cfg, acc.params), _unflat(cfg, acc.m),
+                            _unflat(cfg, acc.v), 1, what="4x16")
+    _check_end_to_end(hp, specs, params, ga, g64, _unflat(cfg, acc.params), p64, cacc, c64)
+    say("oracle forward of sequence 37 of the big batch")
+    _, rr, _ = og.forward(cfg, params, x[37:38], y[37:38])
+    assert np.allclose(rows64[37], rr, rtol=LOSS_TOL, atol=0)
