@@ -228,11 +228,11 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const float* __restric
       }
       bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
       const float m_new = fmaxf(m_run, bmax);
-      const float alpha = exp2f(m_run - m_new);
+      const float alpha = exp2_hw(m_run - m_new);
       float psum = 0.f;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        s[r] = exp2f(s[r] - m_new);
+        s[r] = exp2_hw(s[r] - m_new);
         psum += s[r];
       }
       l_run = l_run * alpha + psum;
@@ -339,7 +339,7 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int key = kv0 + acc_row(r, hh);
-        float p = exp2f(s[r] - lse2);
+        float p = exp2_hw(s[r] - lse2);
         if (need_mask && (key > my_q || key >= sh.T)) p = 0.f;
         s[r] = p * (dp[r] - Dq);  // dS^T
       }
@@ -447,7 +447,7 @@ __global__ void __launch_bounds__(256, 1) attn_bwd_dkv_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int qi = acc_row(r, hh);
-        float p = exp2f(s[r] - sl[qi]);
+        float p = exp2_hw(s[r] - sl[qi]);
         if (need_mask && (my_k > qv0 + qi || my_k >= sh.T)) p = 0.f;
         s[r] = p;
         dp[r] = p * (dp[r] - sd[qi]);

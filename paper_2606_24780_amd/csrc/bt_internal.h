@@ -51,6 +51,12 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// 2^x as the single hardware transcendental (v_exp_f32, about 1 ulp),
+// without the library's rescaling for results below 2^-126: those may come
+// out as 0, an absolute error under 1.2e-38.  Used where the exponent is a
+// softmax logit minus its running maximum, so every result is in [0, 1].
+__device__ __forceinline__ float exp2_hw(float x) { return __builtin_amdgcn_exp2f(x); }
+
 // tanh-form GELU and its derivative (FP32), evaluated through the logistic
 // function: 1 + tanh(u) = 2 s with s = 1 / (1 + exp(-2u)), so
 //   gelu(x)  = x s

@@ -12,9 +12,10 @@
 //    block), 256 threads = 4 waves in a 2 x 2 grid, each wave owns a 64 x 64
 //    sub-tile = 2 x 2 MFMA 32x32 accumulators (64 VGPRs).
 //  * each operand tile is staged global -> VGPR -> LDS with float4 accesses in
-//    the layout of its source (K-contiguous rows [rows][BK+4] or
-//    MN-contiguous rows [BK][128+4]); two LDS buffers, one barrier per k-tile,
-//    the next tile's global loads in flight while the MFMAs run.
+//    the layout of its source (K-contiguous rows [rows][BK] with an XOR chunk
+//    swizzle, or MN-contiguous rows [BK][128+4]); two LDS buffers, one barrier
+//    per k-tile, the next tile's global loads in flight while the MFMAs run,
+//    wave priority raised while a wave issues MFMAs.
 //  * the MFMA k-slot of lane half h at step s is k = 8h + (s mod 8) +
 //    16 (s div 8) (s < BK/2): K-contiguous tiles are read as float4 (4 steps at once),
 //    MN-contiguous tiles as b32 with the two lane halves 8 rows apart, which
@@ -64,8 +65,16 @@ struct GemmParams {
 
 template <bool KC, int BK>
 struct TileSize {
-  static constexpr int value = KC ? BM * (BK + 4) : BK * LDM;
+  static constexpr int value = KC ? BM * BK : BK * LDM;
 };
+
+// K-contiguous tiles are stored unpadded ([rows][BK]) with the 16-byte chunk
+// index of each row XORed by a few row bits: a b128 read of one chunk by 32
+// consecutive rows spreads over all LDS banks without a pad column.
+template <int BK>
+__device__ __forceinline__ int kc_swizzle(int row) {
+  return BK == 16 ? ((row >> 2) & 3) : ((row >> 1) & 7);
+}
 
 // Global -> register staging of one 128 x BK operand tile (BK/8 float4 per
 // thread).  rows = M (or N) extent, kbeg/kend = k range of this split.
@@ -105,7 +114,10 @@ __device__ __forceinline__ void store_tile(float* __restrict__ s, const floatx4 
     constexpr int TPR = BK / 4, RPP = NTHREADS / TPR;
 #pragma unroll
     for (int i = 0; i < BK / 8; ++i)
-      *reinterpret_cast<floatx4*>(s + (tid / TPR + RPP * i) * (BK + 4) + 4 * (tid % TPR)) = r[i];
+      {
+        const int row = tid / TPR + RPP * i;
+        *reinterpret_cast<floatx4*>(s + row * BK + 4 * ((tid % TPR) ^ kc_swizzle<BK>(row))) = r[i];
+      }
   } else {
 #pragma unroll
     for (int i = 0; i < BK / 8; ++i)
@@ -117,7 +129,7 @@ __device__ __forceinline__ void store_tile(float* __restrict__ s, const floatx4 
 template <bool KC, int BK>
 __device__ __forceinline__ floatx4 read_frag(const float* __restrict__ s, int row, int koff) {
   if (KC) {
-    return *reinterpret_cast<const floatx4*>(s + row * (BK + 4) + koff);
+    return *reinterpret_cast<const floatx4*>(s + row * BK + 4 * ((koff >> 2) ^ kc_swizzle<BK>(row)));
   } else {
     floatx4 v;
     v[0] = s[(koff + 0) * LDM + row];
@@ -245,6 +257,10 @@ __global__ void __launch_bounds__(NTHREADS, OCC) gemm_f32_mfma(const GemmParams 
     }
     const float* sA = smem + cur * (A_SZ + B_SZ);
     const float* sB = sA + A_SZ;
+    // raised wave priority while this wave issues its MFMAs, so the
+    // arbiter favours waves that keep the matrix core fed over waves that
+    // are staging the next tile
+    __builtin_amdgcn_s_setprio(1);
 #pragma unroll
     for (int c = 0; c < BK / 8; ++c) {
       const int koff = 8 * hh + 4 * (c & 1) + 16 * (c >> 1);
@@ -262,6 +278,7 @@ __global__ void __launch_bounds__(NTHREADS, OCC) gemm_f32_mfma(const GemmParams 
             acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[mb][q], fb[nb][q], acc[mb][nb],
                                                                0, 0, 0);
     }
+    __builtin_amdgcn_s_setprio(0);
     if (more) {
       if (COLSUM)
 #pragma unroll

@@ -64,7 +64,7 @@ __global__ void __launch_bounds__(XT) xent_row_kernel(float* logits, const int32
   for (int i = 0; i < NPT; ++i)
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      z[i][k] = exp2f(z[i][k] * LOG2E_X - mxl);
+      z[i][k] = exp2_hw(z[i][k] * LOG2E_X - mxl);
       s += z[i][k];
     }
   s = block_reduce(s, red, false);
@@ -108,7 +108,7 @@ __global__ void __launch_bounds__(256) xent_bwd_kernel(const float* logits, cons
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int c = 4 * c4 + k;
-      o[k] = c < V ? (exp2f((z[k] - l) * LOG2E_X) - (c == y ? 1.f : 0.f)) * scale : 0.f;
+      o[k] = c < V ? (exp2_hw((z[k] - l) * LOG2E_X) - (c == y ? 1.f : 0.f)) * scale : 0.f;
     }
     dr[c4] = o;
   }
