@@ -41,16 +41,28 @@ def parse():
     return ap.parse_args()
 
 
+def code_sha256(path):
+    """sha256 of a source file's code: // comments, trailing blanks and empty
+    lines removed, so that comment edits do not count as kernel changes."""
+    import hashlib
+    import re
+    lines = []
+    for line in open(path, encoding="utf-8"):
+        line = re.sub(r"//.*$", "", line).rstrip()
+        if line:
+            lines.append(line)
+    return hashlib.sha256("\n".join(lines).encode()).hexdigest()
+
+
 def gemm_traffic():
     """HBM bytes per GEMM launch from the committed rocprofv3 FETCH_SIZE /
     WRITE_SIZE passes (scaled by a plain 1 GiB copy), or None when the GEMM
-    source has changed since the counters were taken."""
-    import hashlib
+    code has changed since the counters were taken."""
     path = os.path.join(ROOT, "profiles", "gemm_f32_mfma_gpt2_124m_b16_traffic.json")
     src = os.path.join(ROOT, "paper_2606_24780_amd", "csrc", "gemm.hip")
     try:
         rec = json.load(open(path))
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()
+        sha = code_sha256(src)
     except (OSError, ValueError):
         return None, None
     if rec.get("gemm_source_sha256") != sha:

@@ -7,40 +7,46 @@
 // gradient dW = X^T dY (TN, reduction over tokens, split along K).
 //
 // Design (gfx950):
-//  * block tile 128 x 128 x BK (BK = 32 at 2 blocks per CU, or BK = 16 at 3-4
-//    blocks per CU for shapes whose tile count would leave CUs with a lone
-//    block), 256 threads = 4 waves in a 2 x 2 grid, each wave owns a 64 x 64
-//    sub-tile = 2 x 2 MFMA 32x32 accumulators (64 VGPRs).
-//  * each operand tile is staged global -> VGPR -> LDS with float4 accesses in
-//    the layout of its source (K-contiguous rows [rows][BK] with an XOR chunk
-//    swizzle, or MN-contiguous rows [BK][128+4]); two LDS buffers, one barrier
-//    per k-tile, the next tile's global loads in flight while the MFMAs run,
-//    wave priority raised while a wave issues MFMAs.
+//  * block tile 128 x 128 x BK (BK = 16 at 4 blocks per CU, or BK = 32 at 2),
+//    256 threads = 4 waves in a 2 x 2 grid, each wave owns a 64 x 64 sub-tile
+//    = 2 x 2 MFMA 32x32 accumulators (64 VGPRs).  The kernel is written for
+//    any WM x WN wave grid; 256 x 128, 128 x 256 and 256 x 256 block tiles were
+//    measured no faster on the model's shapes and are not launched.
+//  * when every tile of a launch is full (M, N multiples of 128, K range a
+//    multiple of BK: all GPT-2 shapes) operand tiles go straight from global
+//    memory into LDS (global_load_lds_dwordx4, 1 KB per wave instruction):
+//    no staging VGPRs, no LDS store instructions.  Ragged shapes stage them
+//    global -> VGPR -> LDS with bounds checks.  On MI355X the direct copies
+//    raised the matrix-pipe busy fraction of the NN / TN products by 3-5
+//    points (measured with SQ_VALU_MFMA_BUSY_CYCLES).
+//  * LDS layouts follow the source layout: K-contiguous rows [rows][BK] with
+//    an XOR swizzle of 16-byte chunks; MN-contiguous rows [BK][128] with the
+//    32-column halves swapped in every other group of 8 k-rows (direct copy)
+//    or padded to [BK][132] (staged).  Two LDS buffers, one barrier per
+//    k-tile, the next tile in flight while the MFMAs run, wave priority
+//    raised while a wave issues MFMAs.
 //  * the MFMA k-slot of lane half h at step s is k = 8h + (s mod 8) +
-//    16 (s div 8) (s < BK/2): K-contiguous tiles are read as float4 (4 steps at once),
-//    MN-contiguous tiles as b32 with the two lane halves 8 rows apart, which
-//    keeps both reads free of LDS bank conflicts.
+//    16 (s div 8) (s < BK/2): K-contiguous tiles are read as float4 (4 steps
+//    at once), MN-contiguous tiles as b32 with the two lane halves 8 rows
+//    apart; both reads are free of LDS bank conflicts.
 //  * blocks are remapped so that each XCD (round-robin dispatch over 8 XCDs,
 //    one L2 each) receives a contiguous range of a grouped (8 tile-rows)
 //    tile order, so concurrently running tiles share A rows / B columns in L2.
 //  * low-parallelism weight-gradient shapes (small M x N, long K) are split
 //    along K; partials go to a workspace and are summed in a fixed order.
-//    Tile depth, occupancy and split count are chosen per shape from a model
-//    of how the blocks land on the 256 CUs (blocks per CU, resident blocks).
+//    Tile depth and split count are chosen per shape from a model of how
+//    the blocks land on the 256 CUs (blocks per CU, resident blocks).
 //  * fused epilogues: bias, bias + tanh-GELU (optionally storing the
 //    pre-activation), GELU-backward (multiply by gelu'(pre)), residual add and
 //    beta = 1 accumulation.
 //  * the weight-gradient product can also return the column sums of dY (the
-//    bias gradient) from the B tiles it already stages, so the bias gradient
+//    bias gradient) from the B data it already reads, so the bias gradient
 //    costs no extra pass over dY.
 #include "bt_internal.h"
 
 namespace bt {
 namespace {
 
-constexpr int BM = 128, BN = 128;
-constexpr int LDM = BM + 4;   // row stride of MN-contiguous LDS tiles (BM == BN)
-constexpr int NTHREADS = 256;
 constexpr int NUM_CU = 256;
 constexpr size_t MAX_SPLIT_WS = (size_t)1 << 30;  // largest split-K partial buffer considered
 
@@ -63,9 +69,20 @@ struct GemmParams {
   float beta;
 };
 
-template <bool KC, int BK>
+// LDS floats of one R-row operand tile: K-contiguous [R][BK] (swizzled) or
+// MN-contiguous [BK][R + 4] (the pad keeps the two lane halves, 8 k-rows
+// apart, on different banks); MN-contiguous tiles copied directly into LDS
+// are unpadded [BK][R] with an XOR swizzle instead.
+template <bool KC, int R, int BK, bool DTL>
 struct TileSize {
-  static constexpr int value = KC ? BM * BK : BK * LDM;
+  static constexpr int value = KC ? R * BK : BK * (DTL ? R : R + 4);
+};
+
+// float4 registers per thread that stage one R-row operand tile
+template <int R, int BK, int NT>
+struct TileVecs {
+  static constexpr int value = R * BK / (4 * NT);
+  static_assert(value >= 1 && R * BK == value * 4 * NT, "tile does not divide over the block");
 };
 
 // K-contiguous tiles are stored unpadded ([rows][BK]) with the 16-byte chunk
@@ -76,18 +93,69 @@ __device__ __forceinline__ int kc_swizzle(int row) {
   return BK == 16 ? ((row >> 2) & 3) : ((row >> 1) & 7);
 }
 
-// Global -> register staging of one 128 x BK operand tile (BK/8 float4 per
+// Unpadded MN-contiguous tiles: in k-rows with bit 3 set the two 32-column
+// halves of every 64-column group trade places, so a fragment read (lane
+// halves 8 k-rows apart, 32 consecutive columns each) hits distinct banks.
+__device__ __forceinline__ int mn_swizzle(int k) { return ((k >> 3) & 1) << 5; }
+
+// Direct global -> LDS copy of 16 bytes per lane (gfx950 global_load_lds_dwordx4):
+// lane L of the wave writes LDS bytes [dst + 16 L, dst + 16 L + 16), dst
+// wave-uniform, passed in M0.  The data never occupies VGPRs and needs no
+// LDS store instruction.  It is issued from inline assembly so that the
+// compiler does not conservatively wait for it before unrelated LDS reads
+// of the other buffer; completion is awaited explicitly (wait_copies) before
+// the barrier that publishes the tile.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void copy16_to_lds(const float* src, float* lds_dst) {
+  const unsigned l = (unsigned)(uintptr_t)(__attribute__((address_space(3))) float*)lds_dst;
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(__builtin_amdgcn_readfirstlane(l)), "v"(src)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+__device__ __forceinline__ void wait_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Per-lane sources of the NI direct copies (1 KB slices) a wave issues for
+// one R x BK operand tile at k = k0; later tiles add a fixed stride.
+template <bool KC, int R, int BK, int NI>
+__device__ __forceinline__ void copy_setup(const float* (&g)[NI], const float* __restrict__ X, long long ld,
+                                           int row0, int k0, int wave, int lane) {
+#pragma unroll
+  for (int j = 0; j < NI; ++j) {
+    const int slice = wave * NI + j;
+    if (KC) {
+      constexpr int TPR = BK / 4, RPS = 64 / TPR;  // rows per 1 KB slice
+      const int row = slice * RPS + lane / TPR;
+      const int q = (lane % TPR) ^ kc_swizzle<BK>(row);
+      g[j] = X + (long long)(row0 + row) * ld + k0 + 4 * q;
+    } else {
+      constexpr int LPK = R / 4, KPS = 64 / LPK;  // lanes per k-row, k-rows per slice
+      const int k = slice * KPS + lane / LPK;
+      const int col = (4 * (lane % LPK)) ^ mn_swizzle(k);
+      g[j] = X + (long long)(k0 + k) * ld + row0 + col;
+    }
+  }
+}
+
+template <int NI>
+__device__ __forceinline__ void copy_issue(const float* const (&g)[NI], long long adv, float* tile, int wave) {
+#pragma unroll
+  for (int j = 0; j < NI; ++j) copy16_to_lds(g[j] + adv, tile + (wave * NI + j) * 256);
+}
+
+// Global -> register staging of one R x BK operand tile (NV float4 per
 // thread).  rows = M (or N) extent, kbeg/kend = k range of this split.
-template <bool KC, int BK>
-__device__ __forceinline__ void load_tile(floatx4 (&r)[BK / 8], const float* __restrict__ X,
-                                          long long ld, int row0, int rows, int k0, int kend,
-                                          int tid) {
+template <bool KC, int R, int BK, int NT, int NV = TileVecs<R, BK, NT>::value>
+__device__ __forceinline__ void load_tile(floatx4 (&r)[NV], const float* __restrict__ X, long long ld,
+                                          int row0, int rows, int k0, int kend, int tid) {
   if (KC) {
     // [rows][K]: BK/4 threads per row, 4 consecutive k each (BK*4 bytes per row)
-    constexpr int TPR = BK / 4, RPP = NTHREADS / TPR;
+    constexpr int TPR = BK / 4, RPP = NT / TPR;
     const int kk = k0 + 4 * (tid % TPR);
 #pragma unroll
-    for (int i = 0; i < BK / 8; ++i) {
+    for (int i = 0; i < NV; ++i) {
       const int row = row0 + tid / TPR + RPP * i;
       if (row < rows && kk < kend)
         r[i] = *reinterpret_cast<const floatx4*>(X + (long long)row * ld + kk);
@@ -95,11 +163,12 @@ __device__ __forceinline__ void load_tile(floatx4 (&r)[BK / 8], const float* __r
         r[i] = floatx4{0.f, 0.f, 0.f, 0.f};
     }
   } else {
-    // [K][rows]: thread -> (k = tid/32 + 8 i, col = 4 (tid%32)); 512 B per k row
-    const int col = row0 + 4 * (tid & 31);
+    // [K][rows]: R/4 threads per k row, thread -> (k = tid / TPK + KPP i, col = 4 (tid % TPK))
+    constexpr int TPK = R / 4, KPP = NT / TPK;
+    const int col = row0 + 4 * (tid % TPK);
 #pragma unroll
-    for (int i = 0; i < BK / 8; ++i) {
-      const int kk = k0 + (tid >> 5) + 8 * i;
+    for (int i = 0; i < NV; ++i) {
+      const int kk = k0 + tid / TPK + KPP * i;
       if (kk < kend && col < rows)
         r[i] = *reinterpret_cast<const floatx4*>(X + (long long)kk * ld + col);
       else
@@ -108,26 +177,35 @@ __device__ __forceinline__ void load_tile(floatx4 (&r)[BK / 8], const float* __r
   }
 }
 
-template <bool KC, int BK>
-__device__ __forceinline__ void store_tile(float* __restrict__ s, const floatx4 (&r)[BK / 8], int tid) {
+template <bool KC, int R, int BK, int NT, int NV = TileVecs<R, BK, NT>::value>
+__device__ __forceinline__ void store_tile(float* __restrict__ s, const floatx4 (&r)[NV], int tid) {
   if (KC) {
-    constexpr int TPR = BK / 4, RPP = NTHREADS / TPR;
+    constexpr int TPR = BK / 4, RPP = NT / TPR;
 #pragma unroll
-    for (int i = 0; i < BK / 8; ++i)
-      {
-        const int row = tid / TPR + RPP * i;
-        *reinterpret_cast<floatx4*>(s + row * BK + 4 * ((tid % TPR) ^ kc_swizzle<BK>(row))) = r[i];
-      }
+    for (int i = 0; i < NV; ++i) {
+      const int row = tid / TPR + RPP * i;
+      *reinterpret_cast<floatx4*>(s + row * BK + 4 * ((tid % TPR) ^ kc_swizzle<BK>(row))) = r[i];
+    }
   } else {
+    constexpr int TPK = R / 4, KPP = NT / TPK;
 #pragma unroll
-    for (int i = 0; i < BK / 8; ++i)
-      *reinterpret_cast<floatx4*>(s + ((tid >> 5) + 8 * i) * LDM + 4 * (tid & 31)) = r[i];
+    for (int i = 0; i < NV; ++i)
+      *reinterpret_cast<floatx4*>(s + (tid / TPK + KPP * i) * (R + 4) + 4 * (tid % TPK)) = r[i];
   }
 }
 
 // Fragment for 4 consecutive MFMA steps (chunk c) of one 32-row block.
-template <bool KC, int BK>
+template <bool KC, int R, int BK, bool DTL>
 __device__ __forceinline__ floatx4 read_frag(const float* __restrict__ s, int row, int koff) {
+  constexpr int LDM = DTL ? R : R + 4;
+  if (!KC && DTL) {
+    floatx4 v;
+    v[0] = s[(koff + 0) * LDM + (row ^ mn_swizzle(koff + 0))];
+    v[1] = s[(koff + 1) * LDM + (row ^ mn_swizzle(koff + 1))];
+    v[2] = s[(koff + 2) * LDM + (row ^ mn_swizzle(koff + 2))];
+    v[3] = s[(koff + 3) * LDM + (row ^ mn_swizzle(koff + 3))];
+    return v;
+  }
   if (KC) {
     return *reinterpret_cast<const floatx4*>(s + row * BK + 4 * ((koff >> 2) ^ kc_swizzle<BK>(row)));
   } else {
@@ -188,11 +266,24 @@ __device__ __forceinline__ void epilogue_block(const GemmParams& p, const floatx
   }
 }
 
-template <bool A_KC, bool B_KC, int EPI, bool SPLIT, bool COLSUM, int BK, int OCC>
-__global__ void __launch_bounds__(NTHREADS, OCC) gemm_f32_mfma(const GemmParams p) {
-  constexpr int A_SZ = TileSize<A_KC, BK>::value;
-  constexpr int B_SZ = TileSize<B_KC, BK>::value;
-  constexpr int NLD = BK / 8;  // float4 staged per thread per operand
+// WM x WN waves, each owning a 64 x 64 output sub-tile: block tile
+// (64 WM) x (64 WN), 64 WM WN threads.  DTL: every tile of the launch is
+// full (M, N multiples of the block tile, K range a multiple of BK), and
+// operand tiles are copied straight from global memory into LDS; otherwise
+// they are staged through registers with bounds checks (ragged shapes).
+template <bool A_KC, bool B_KC, int EPI, bool SPLIT, bool COLSUM, int BK, int OCC, int WM, int WN, bool DTL>
+__global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmParams p) {
+  constexpr int BM = 64 * WM, BN = 64 * WN, NW = WM * WN, NT = 64 * NW;
+  constexpr int A_SZ = TileSize<A_KC, BM, BK, DTL>::value;
+  constexpr int B_SZ = TileSize<B_KC, BN, BK, DTL>::value;
+  constexpr int NA = DTL ? 1 : TileVecs<BM, BK, NT>::value;  // float4 staged per thread, A
+  constexpr int NB = DTL ? 1 : TileVecs<BN, BK, NT>::value;  // float4 staged per thread, B
+  constexpr int CA = BM * BK / (256 * NW);  // direct 1 KB copies per wave per tile, A
+  constexpr int CB = BN * BK / (256 * NW);  // direct 1 KB copies per wave per tile, B
+  static_assert(!DTL || (CA >= 1 && CB >= 1 && CA * 256 * NW == BM * BK && CB * 256 * NW == BN * BK),
+                "direct copies must tile the operand tiles in 1 KB slices");
+  static_assert(!DTL || (BM <= 256 && BN <= 256), "an MN-contiguous k-row must fit one wave copy");
+  static_assert(DTL || !COLSUM || 4 * NT <= 2 * (A_SZ + B_SZ), "column-sum combine needs 16 B per thread of LDS");
   static_assert(2 * (A_SZ + B_SZ) * 4 * OCC <= 160 * 1024, "LDS exceeds one CU at this occupancy");
   __shared__ __attribute__((aligned(16))) float smem[2 * (A_SZ + B_SZ)];
 
@@ -201,7 +292,7 @@ __global__ void __launch_bounds__(NTHREADS, OCC) gemm_f32_mfma(const GemmParams 
   const int wave = tid >> 6;
   const int lr = lane & 31;
   const int hh = lane >> 5;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
 
   // ---- tile scheduling: XCD-contiguous ranges of a grouped tile order
   const int ntiles = p.tiles_m * p.tiles_n;
@@ -231,19 +322,37 @@ __global__ void __launch_bounds__(NTHREADS, OCC) gemm_f32_mfma(const GemmParams 
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-  floatx4 ra[NLD], rb[NLD];
-  // Column sums of op(B) (only for MN-contiguous B, i.e. op(B) = B [K][N]):
-  // each thread adds up the B rows it stages, the 8 row groups are combined
-  // at the end.  Only the first tile row of blocks (tm == 0) keeps them.
+  floatx4 ra[NA], rb[NB];
+  const float* ga[CA];
+  const float* gb[CB];
+  const long long a_step = A_KC ? BK : (long long)BK * p.lda;  // per k-tile source advance
+  const long long b_step = B_KC ? BK : (long long)BK * p.ldb;
+  // Column sums of op(B) (only for MN-contiguous B, i.e. op(B) = B [K][N]),
+  // kept only by the first tile row of blocks (tm == 0).  Staged path: each
+  // thread adds up the B rows it stages and the NT / (BN/4) row groups are
+  // combined at the end.  Direct path: each lane adds up the B fragments it
+  // reads (its column, its half of every k-tile) and the lane halves are
+  // combined at the end.
   floatx4 csum = floatx4{0.f, 0.f, 0.f, 0.f};
+  floatx4 csf[2] = {floatx4{0.f, 0.f, 0.f, 0.f}, floatx4{0.f, 0.f, 0.f, 0.f}};
+  if (DTL) {
+    copy_setup<A_KC, BM, BK, CA>(ga, p.A, p.lda, m0, kbeg, wave, lane);
+    copy_setup<B_KC, BN, BK, CB>(gb, p.B, p.ldb, n0, kbeg, wave, lane);
+  }
   if (nk > 0) {
-    load_tile<A_KC, BK>(ra, p.A, p.lda, m0, p.M, kbeg, kend, tid);
-    load_tile<B_KC, BK>(rb, p.B, p.ldb, n0, p.N, kbeg, kend, tid);
-    if (COLSUM)
+    if (DTL) {
+      copy_issue<CA>(ga, 0, smem, wave);
+      copy_issue<CB>(gb, 0, smem + A_SZ, wave);
+      wait_copies();
+    } else {
+      load_tile<A_KC, BM, BK, NT>(ra, p.A, p.lda, m0, p.M, kbeg, kend, tid);
+      load_tile<B_KC, BN, BK, NT>(rb, p.B, p.ldb, n0, p.N, kbeg, kend, tid);
+      if (COLSUM)
 #pragma unroll
-      for (int i = 0; i < NLD; ++i) csum += rb[i];
-    store_tile<A_KC, BK>(smem, ra, tid);
-    store_tile<B_KC, BK>(smem + A_SZ, rb, tid);
+        for (int i = 0; i < NB; ++i) csum += rb[i];
+      store_tile<A_KC, BM, BK, NT>(smem, ra, tid);
+      store_tile<B_KC, BN, BK, NT>(smem + A_SZ, rb, tid);
+    }
   }
   __syncthreads();
 
@@ -251,9 +360,16 @@ __global__ void __launch_bounds__(NTHREADS, OCC) gemm_f32_mfma(const GemmParams 
     const int cur = kt & 1;
     const bool more = kt + 1 < nk;
     if (more) {
-      const int k0 = kbeg + (kt + 1) * BK;
-      load_tile<A_KC, BK>(ra, p.A, p.lda, m0, p.M, k0, kend, tid);
-      load_tile<B_KC, BK>(rb, p.B, p.ldb, n0, p.N, k0, kend, tid);
+      if (DTL) {
+        // the other buffer was last read before the previous barrier
+        float* sN = smem + (cur ^ 1) * (A_SZ + B_SZ);
+        copy_issue<CA>(ga, (kt + 1) * a_step, sN, wave);
+        copy_issue<CB>(gb, (kt + 1) * b_step, sN + A_SZ, wave);
+      } else {
+        const int k0 = kbeg + (kt + 1) * BK;
+        load_tile<A_KC, BM, BK, NT>(ra, p.A, p.lda, m0, p.M, k0, kend, tid);
+        load_tile<B_KC, BN, BK, NT>(rb, p.B, p.ldb, n0, p.N, k0, kend, tid);
+      }
     }
     const float* sA = smem + cur * (A_SZ + B_SZ);
     const float* sB = sA + A_SZ;
@@ -266,9 +382,9 @@ __global__ void __launch_bounds__(NTHREADS, OCC) gemm_f32_mfma(const GemmParams 
       const int koff = 8 * hh + 4 * (c & 1) + 16 * (c >> 1);
       floatx4 fa[2], fb[2];
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) fa[mb] = read_frag<A_KC, BK>(sA, wm * 64 + mb * 32 + lr, koff);
+      for (int mb = 0; mb < 2; ++mb) fa[mb] = read_frag<A_KC, BM, BK, DTL>(sA, wm * 64 + mb * 32 + lr, koff);
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb) fb[nb] = read_frag<B_KC, BK>(sB, wn * 64 + nb * 32 + lr, koff);
+      for (int nb = 0; nb < 2; ++nb) fb[nb] = read_frag<B_KC, BN, BK, DTL>(sB, wn * 64 + nb * 32 + lr, koff);
 #pragma unroll
       for (int q = 0; q < 4; ++q)
 #pragma unroll
@@ -277,36 +393,63 @@ __global__ void __launch_bounds__(NTHREADS, OCC) gemm_f32_mfma(const GemmParams 
           for (int nb = 0; nb < 2; ++nb)
             acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[mb][q], fb[nb][q], acc[mb][nb],
                                                                0, 0, 0);
+      if (DTL && COLSUM) {
+        csf[0] += fb[0];
+        csf[1] += fb[1];
+      }
     }
     __builtin_amdgcn_s_setprio(0);
-    if (more) {
+    if (DTL) {
+      wait_copies();
+    } else if (more) {
       if (COLSUM)
 #pragma unroll
-        for (int i = 0; i < NLD; ++i) csum += rb[i];
+        for (int i = 0; i < NB; ++i) csum += rb[i];
       float* sN = smem + (cur ^ 1) * (A_SZ + B_SZ);
-      store_tile<A_KC, BK>(sN, ra, tid);
-      store_tile<B_KC, BK>(sN + A_SZ, rb, tid);
+      store_tile<A_KC, BM, BK, NT>(sN, ra, tid);
+      store_tile<B_KC, BN, BK, NT>(sN + A_SZ, rb, tid);
     }
     __syncthreads();
   }
 
   if (COLSUM && tm == 0) {
-    // combine the 8 staging row groups (tid / 32) in a fixed order
-    floatx4* red = reinterpret_cast<floatx4*>(smem);
-    red[tid] = csum;
-    __syncthreads();
-    if (tid < 32) {
-      floatx4 s = red[tid];
+    if (DTL) {
+      // waves of the first wave row read every B column of the tile once
+      if (wm == 0) {
 #pragma unroll
-      for (int gi = 1; gi < 8; ++gi) s += red[tid + 32 * gi];
-      const int n = n0 + 4 * tid;
-      if (n < p.N) {
-        if (SPLIT) {
-          *reinterpret_cast<floatx4*>(p.ws_colsum + (long long)z * p.N + n) = s;
-        } else {
-          floatx4* d = reinterpret_cast<floatx4*>(p.colsum + n);
-          if (p.beta != 0.f) s += *d;
-          *d = s;
+        for (int nb = 0; nb < 2; ++nb) {
+          float v = (csf[nb][0] + csf[nb][1]) + (csf[nb][2] + csf[nb][3]);
+          v += __shfl_xor(v, 32, 64);
+          const int n = n0 + wn * 64 + nb * 32 + lr;
+          if (hh == 0 && n < p.N) {
+            if (SPLIT) {
+              p.ws_colsum[(long long)z * p.N + n] = v;
+            } else {
+              if (p.beta != 0.f) v += p.colsum[n];
+              p.colsum[n] = v;
+            }
+          }
+        }
+      }
+    } else {
+      // combine the staging row groups (tid / (BN/4)) in a fixed order
+      constexpr int TPK = BN / 4, GROUPS = NT / TPK;
+      floatx4* red = reinterpret_cast<floatx4*>(smem);
+      red[tid] = csum;
+      __syncthreads();
+      if (tid < TPK) {
+        floatx4 s = red[tid];
+#pragma unroll
+        for (int gi = 1; gi < GROUPS; ++gi) s += red[tid + TPK * gi];
+        const int n = n0 + 4 * tid;
+        if (n < p.N) {
+          if (SPLIT) {
+            *reinterpret_cast<floatx4*>(p.ws_colsum + (long long)z * p.N + n) = s;
+          } else {
+            floatx4* d = reinterpret_cast<floatx4*>(p.colsum + n);
+            if (p.beta != 0.f) s += *d;
+            *d = s;
+          }
         }
       }
     }
@@ -363,37 +506,49 @@ __global__ void __launch_bounds__(256) splitk_colsum_reduce(const float* __restr
   out[n] = s;
 }
 
-struct GemmCfg {
-  int bk, occ, splits, ksplit;
+// Block-tile configurations: tile depth, wave grid (64 x 64 outputs per
+// wave), resident blocks per CU, and the relative rate of one CU working
+// through 128 x 128 x 16 tile steps when it holds its full complement of
+// blocks (K-contiguous operand present / both operands MN-contiguous),
+// measured on MI355X.  Larger block tiles (256 x 128, 128 x 256, 256 x 256)
+// were measured no faster on these shapes and are not offered.
+struct TileCfg {
+  int bk, wm, wn, occ;
+  double rate_kc, rate_mn;
 };
+constexpr TileCfg kTileCfgs[] = {
+    {32, 2, 2, 2, 1.00, 1.00},
+    {16, 2, 2, 4, 1.0 / 0.95, 1.0 / 0.98},
+};
+constexpr int NUM_TILE_CFGS = (int)(sizeof(kTileCfgs) / sizeof(kTileCfgs[0]));
 
-// Blocks per CU that can stay resident for a layout and tile depth.
-int occupancy_for(int bk, bool akc, bool bkc) {
-  if (bk == 32) return 2;
-  return (akc && bkc) ? 3 : 4;  // two K-contiguous 128 x 20 tiles need 41 KB
-}
+struct GemmCfg {
+  int tc;  // index into kTileCfgs
+  int splits, ksplit;
+};
 
 // Relative time of a launch of `blocks` equal blocks (each `work` long): the
 // busiest CU holds ceil(blocks / NUM_CU) of them and runs up to `occ` at
-// once; a lone resident 4-wave block keeps the matrix pipe only partly busy
-// (taken as 60%).
-double launch_time(long long blocks, int occ, double work) {
+// once.  A last round with only one wave per SIMD resident keeps the matrix
+// pipe only partly busy (taken as 60%).
+double launch_time(long long blocks, int occ, int waves_per_block, double work) {
   const long long per_cu = (blocks + NUM_CU - 1) / NUM_CU;
   const long long full = per_cu / occ, rem = per_cu % occ;
   double t = (double)(full * occ) * work;
-  if (rem) t += (double)rem * work / (rem >= 2 ? 1.0 : 0.6);
+  if (rem) t += (double)rem * work / (rem * waves_per_block >= 8 ? 1.0 : 0.6);
   return t;
 }
 
-// Tile depth, occupancy and K split for a shape.  Split-K (only for products
+// Tile configuration and K split for a shape.  Split-K (only for products
 // without an epilogue) adds a partial-tile round trip through the workspace.
 GemmCfg choose_config(int M, int N, int K, bool akc, bool bkc, bool may_split) {
-  if (K <= 0) return GemmCfg{32, 2, 1, 32};
-  const long long tiles = (long long)((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-  GemmCfg best{32, 2, 1, K};
+  if (K <= 0) return GemmCfg{0, 1, 32};
+  GemmCfg best{0, 1, K};
   double best_t = 1e300;
-  for (int bk : {32, 16}) {
-    const int occ = occupancy_for(bk, akc, bkc);
+  for (int tc = 0; tc < NUM_TILE_CFGS; ++tc) {
+    const TileCfg& c = kTileCfgs[tc];
+    const int bm = 64 * c.wm, bn = 64 * c.wn, bk = c.bk;
+    const long long tiles = (long long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     const int kt = (K + bk - 1) / bk;
     int smax = 1;
     if (may_split && K >= 8 * bk) smax = kt / 4 < 32 ? kt / 4 : 32;
@@ -402,57 +557,60 @@ GemmCfg choose_config(int M, int N, int K, bool akc, bool bkc, bool may_split) {
       ks = (ks + bk - 1) / bk * bk;
       if ((K + ks - 1) / ks != s) continue;
       if (s > 1 && (double)s * M * N * sizeof(float) > (double)MAX_SPLIT_WS) continue;
-      // time in 128 x 128 x 16 tile steps.  Measured on MI355X: with a
-      // K-contiguous operand, BK = 16 at 3-4 resident blocks runs each step
-      // about 5% faster than BK = 32 at 2 (more waves hide the barriers);
-      // with both operands MN-contiguous the gain is about 2%.
-      const double work = (double)ks / 16.0 * (bk == 16 ? ((akc || bkc) ? 0.95 : 0.98) : 1.0);
-      double t = launch_time(tiles * s, occ, work);
-      if (s > 1) t += 4.0 * (double)s * tiles / NUM_CU;  // partial tiles out and back
+      // time in 128 x 128 x 16 tile steps of a full CU
+      const double work = (double)bm * bn / (128.0 * 128.0) * ks / 16.0 / ((akc || bkc) ? c.rate_kc : c.rate_mn);
+      double t = launch_time(tiles * s, c.occ, c.wm * c.wn, work);
+      if (s > 1) t += 4.0 * (double)s * M * N / (128.0 * 128.0) / NUM_CU;  // partial tiles out and back
       if (t < best_t * 0.995) {
         best_t = t;
-        best = GemmCfg{bk, occ, s, ks};
+        best = GemmCfg{tc, s, ks};
       }
     }
   }
   return best;
 }
 
-template <bool A_KC, bool B_KC, int BK, int OCC>
+template <bool A_KC, bool B_KC, int BK, int OCC, int WM, int WN, bool DTL>
 void launch_cfg(const GemmParams& p, int epi, bool split, dim3 grid, hipStream_t s) {
   const bool cs = p.colsum != nullptr;
+  const dim3 block(64 * WM * WN);
   if (split) {
     if (cs)
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, !B_KC, BK, OCC>), grid, dim3(NTHREADS), 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, !B_KC, BK, OCC, WM, WN, DTL>), grid, block, 0, s, p);
     else
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, false, BK, OCC>), grid, dim3(NTHREADS), 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, false, BK, OCC, WM, WN, DTL>), grid, block, 0, s, p);
     return;
   }
   switch (epi) {
     case BT_EPI_NONE:
       if (cs)
-        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, !B_KC, BK, OCC>), grid, dim3(NTHREADS), 0, s, p);
+        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, !B_KC, BK, OCC, WM, WN, DTL>), grid, block, 0, s, p);
       else
-        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, false, BK, OCC>), grid, dim3(NTHREADS), 0, s, p);
+        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, false, BK, OCC, WM, WN, DTL>), grid, block, 0, s, p);
       break;
     case BT_EPI_BIAS:
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS, false, false, BK, OCC>), grid, dim3(NTHREADS), 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS, false, false, BK, OCC, WM, WN, DTL>), grid, block, 0, s, p);
       break;
     case BT_EPI_BIAS_GELU:
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS_GELU, false, false, BK, OCC>), grid, dim3(NTHREADS), 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS_GELU, false, false, BK, OCC, WM, WN, DTL>), grid, block, 0, s, p);
       break;
     default:
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_DGELU, false, false, BK, OCC>), grid, dim3(NTHREADS), 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_DGELU, false, false, BK, OCC, WM, WN, DTL>), grid, block, 0, s, p);
       break;
   }
 }
 
+// dtl: every tile is full, so operand tiles are copied directly into LDS
 template <bool A_KC, bool B_KC>
-void launch_layout(const GemmParams& p, const GemmCfg& c, int epi, bool split, dim3 grid, hipStream_t s) {
-  if (c.bk == 32)
-    launch_cfg<A_KC, B_KC, 32, 2>(p, epi, split, grid, s);
-  else
-    launch_cfg<A_KC, B_KC, 16, (A_KC && B_KC) ? 3 : 4>(p, epi, split, grid, s);
+void launch_layout(const GemmParams& p, const GemmCfg& c, int epi, bool split, bool dtl, dim3 grid,
+                   hipStream_t s) {
+  if (c.tc == 0) {
+    if (dtl) launch_cfg<A_KC, B_KC, 32, 2, 2, 2, true>(p, epi, split, grid, s);
+    else launch_cfg<A_KC, B_KC, 32, 2, 2, 2, false>(p, epi, split, grid, s);
+  } else {
+    if (dtl) launch_cfg<A_KC, B_KC, 16, 4, 2, 2, true>(p, epi, split, grid, s);
+    else launch_cfg<A_KC, B_KC, 16, 4, 2, 2, false>(p, epi, split, grid, s);
+  }
 }
 
 }  // namespace
@@ -514,12 +672,13 @@ extern "C" bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K, const fl
   p.N = N;
   p.K = K;
   p.beta = beta;
-  p.tiles_m = (M + BM - 1) / BM;
-  p.tiles_n = (N + BN - 1) / BN;
   const bool may_split = epi == BT_EPI_NONE && residual == nullptr;
   const bool akc = opA == BT_OP_N;
   const bool bkc = opB == BT_OP_T;
   const GemmCfg cfg = choose_config(M, N, K, akc, bkc, may_split);
+  const int bm = 64 * kTileCfgs[cfg.tc].wm, bn = 64 * kTileCfgs[cfg.tc].wn;
+  p.tiles_m = (M + bm - 1) / bm;
+  p.tiles_n = (N + bn - 1) / bn;
   const int splits = cfg.splits;
   p.ksplit = cfg.ksplit;
   p.splits = splits;
@@ -536,10 +695,12 @@ extern "C" bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K, const fl
   BT_RETURN_IF(nblocks > 0x7fffffffLL, BT_ESHAPE, "bt_gemm: too many tiles");
   dim3 grid((unsigned)nblocks);
   hipStream_t s = as_stream(stream);
-  if (akc && !bkc) launch_layout<true, false>(p, cfg, epi, split, grid, s);
-  else if (akc && bkc) launch_layout<true, true>(p, cfg, epi, split, grid, s);
-  else if (!akc && !bkc) launch_layout<false, false>(p, cfg, epi, split, grid, s);
-  else launch_layout<false, true>(p, cfg, epi, split, grid, s);
+  const int bk = kTileCfgs[cfg.tc].bk;
+  const bool dtl = M % bm == 0 && N % bn == 0 && K % bk == 0;
+  if (akc && !bkc) launch_layout<true, false>(p, cfg, epi, split, dtl, grid, s);
+  else if (akc && bkc) launch_layout<true, true>(p, cfg, epi, split, dtl, grid, s);
+  else if (!akc && !bkc) launch_layout<false, false>(p, cfg, epi, split, dtl, grid, s);
+  else launch_layout<false, true>(p, cfg, epi, split, dtl, grid, s);
   BT_TRY(check_launch("gemm_f32_mfma"));
   if (split) {
     const long long n4 = (long long)M * (N / 4);

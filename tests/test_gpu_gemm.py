@@ -36,7 +36,8 @@ def _run(torch, ta, tb, M, N, K, A, B, **kw):
 
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
 @pytest.mark.parametrize("M,N,K", [(260, 196, 132), (64, 64, 256), (4, 8, 4), (300, 388, 1000),
-                                   (128, 128, 32), (132, 260, 36), (8, 12, 4096)])
+                                   (128, 128, 32), (132, 260, 36), (8, 12, 4096),
+                                   (256, 384, 272), (384, 256, 1024)])
 def test_gemm_layouts(ta, tb, M, N, K):
     torch = torch_gpu()
     say(f"gemm layout ta={ta} tb={tb} M={M} N={N} K={K}")
@@ -45,9 +46,11 @@ def test_gemm_layouts(ta, tb, M, N, K):
     assert_close_maxabs(host(C), ops.gemm(A, B, bool(ta), bool(tb)), TOL, f"gemm {ta}{tb} {M}x{N}x{K}")
 
 
-def test_gemm_epilogues():
+# (260, 196, 132) has ragged tiles (operands staged through registers); the
+# full-tile shape takes the direct global -> LDS copy path.
+@pytest.mark.parametrize("M,N,K", [(260, 196, 132), (256, 256, 144)])
+def test_gemm_epilogues(M, N, K):
     torch = torch_gpu()
-    M, N, K = 260, 196, 132
     A, B = _operands(M, N, K, 0, 0)
     bias = RNG.standard_normal(N).astype(np.float32)
     res = RNG.standard_normal((M, N)).astype(np.float32)
@@ -74,6 +77,26 @@ def test_gemm_epilogues():
     C = _run(torch, 0, 0, 8, 8, 0, np.zeros((8, 0), np.float32), np.zeros((0, 8), np.float32),
              bias=dev(torch, bias[:8]), epi=bt.EPI_BIAS)
     assert np.array_equal(host(C), np.broadcast_to(bias[:8].astype(np.float64), (8, 8)))
+
+
+@pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
+def test_gemm_full_tiles_match_ragged_path(ta, tb):
+    """A full-tile product (direct LDS copies) and the same data inside a
+    ragged product (register staging) add the same terms in the same order,
+    so the shared 256 x 256 block of C is bitwise equal.  A zero bias keeps
+    both products from being split along K (the split count could differ
+    between the two shapes) and adds exactly 0."""
+    torch = torch_gpu()
+    say(f"gemm full vs ragged path ta={ta} tb={tb}")
+    M, N, K = 256, 256, 512
+    A, B = _operands(M + 4, N + 4, K, ta, tb)
+    zb = torch.zeros(N + 4, dtype=torch.float32, device="cuda")
+    C_big = host(_run(torch, ta, tb, M + 4, N + 4, K, A, B, bias=zb, epi=bt.EPI_BIAS))
+    A_s = np.ascontiguousarray(A[:, :M] if ta else A[:M])
+    B_s = np.ascontiguousarray(B[:N] if tb else B[:, :N])
+    C_small = host(_run(torch, ta, tb, M, N, K, A_s, B_s, bias=zb[:N], epi=bt.EPI_BIAS))
+    assert np.array_equal(C_small, C_big[:M, :N])
+    assert_close_maxabs(C_small, ops.gemm(A_s, B_s, bool(ta), bool(tb)), TOL, "full tiles")
 
 
 def test_gemm_deterministic_split():
