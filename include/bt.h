@@ -113,13 +113,23 @@ bt_status bt_attention_fwd(const float* qkv, float* out, float* lse,
 /*
  * Causal attention backward (appendix "Attention Backward").  From dout
  * [B, T, H, hd], qkv, out and lse of the forward it writes dqkv [B, T, 3, H,
- * hd] (overwritten).  P is recomputed from lse.  ws holds
- * bt_attention_bwd_ws_bytes() bytes (row sums of dout * out).
+ * hd] (overwritten).  P is recomputed from lse.  Deterministic (no atomics).
+ * ws (16-byte aligned, caller-owned, contents scratch) selects the method:
+ *  - ws_bytes >= bt_attention_bwd_ws_bytes(): the row sums D = rowsum(dout *
+ *    out), then a key-major pass that accumulates dK, dV and stores
+ *    dS / sqrt(hd) ([B, H, T, T] floats in ws), then dQ = dS K as one batched
+ *    product.  Needs T % 4 == 0; for other T the size function returns the
+ *    minimum and the second method runs.
+ *  - bt_attention_bwd_ws_min_bytes() <= ws_bytes < that: a query-major pass
+ *    (D and dQ, recomputing S and dP) and the key-major pass (dK, dV); no
+ *    memory quadratic in T.
+ * Smaller (or NULL) ws: BT_EWORKSPACE.
  */
 bt_status bt_attention_bwd(const float* dout, const float* qkv, const float* out,
                            const float* lse, float* dqkv, void* ws, size_t ws_bytes,
                            int B, int T, int H, int hd, void* stream);
 size_t bt_attention_bwd_ws_bytes(int B, int T, int H, int hd);
+size_t bt_attention_bwd_ws_min_bytes(int B, int T, int H, int hd);
 
 /*
  * LayerNorm forward over the last dimension (pre-normalised blocks of the

@@ -65,6 +65,7 @@ _SIGS = {
     "bt_attention_fwd": (i32, [vp, vp, vp, i32, i32, i32, i32, vp]),
     "bt_attention_bwd": (i32, [vp, vp, vp, vp, vp, vp, sz, i32, i32, i32, i32, vp]),
     "bt_attention_bwd_ws_bytes": (sz, [i32, i32, i32, i32]),
+    "bt_attention_bwd_ws_min_bytes": (sz, [i32, i32, i32, i32]),
     "bt_layernorm_fwd": (i32, [vp, vp, vp, vp, vp, vp, i32, i32, f32, vp]),
     "bt_layernorm_bwd": (i32, [vp, vp, vp, vp, vp, vp, vp, vp, f32, f32, vp, sz, i32, i32, vp]),
     "bt_layernorm_bwd_ws_bytes": (sz, [i32, i32]),
@@ -181,9 +182,11 @@ def bt_attention_fwd(qkv, out, lse, B, T, H, hd, stream=None):
            "bt_attention_fwd")
 
 
-def bt_attention_bwd(dout, qkv, out, lse, dqkv, B, T, H, hd, ws=None, stream=None):
+def bt_attention_bwd(dout, qkv, out, lse, dqkv, B, T, H, hd, ws=None, stream=None, small_ws=False):
+    """small_ws: allocate only bt_attention_bwd_ws_min_bytes (the method that
+    recomputes S and dP for dQ instead of storing dS)."""
     L = lib()
-    need = L.bt_attention_bwd_ws_bytes(B, T, H, hd)
+    need = (L.bt_attention_bwd_ws_min_bytes if small_ws else L.bt_attention_bwd_ws_bytes)(B, T, H, hd)
     w = _ws(need, ws, qkv.device)
     _check(L.bt_attention_bwd(_p(dout), _p(qkv), _p(out), _p(lse), _p(dqkv), _p(w),
                               0 if w is None else w.numel() * w.element_size(), B, T, H, hd,

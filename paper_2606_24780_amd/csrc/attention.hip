@@ -25,8 +25,14 @@
 //    operand of O^T += V^T P^T (k-slot of register r: row 8(r/4) + 4 h + r%4).
 //  * exp is computed as exp2 with log2(e)/sqrt(hd) folded into the register
 //    operand.
-//  * backward is deterministic: one query-major kernel (D, dQ) and one
-//    key-major kernel (dK, dV), each recomputing P from lse; no atomics.
+//  * backward is deterministic (no atomics).  With the full workspace:
+//    D = rowsum(dO o O) in a small kernel, then one key-major kernel
+//    recomputes P from lse, accumulates dK and dV and also writes dS / sqrt(hd)
+//    to the workspace (B H T T floats), and dQ = dS K is one batched product
+//    on the GEMM kernel (causal: each 128-row tile sums only keys below its
+//    end).  This drops the second recomputation of S and dP that a separate
+//    query-major dQ kernel needs.  With only the small workspace, a query-major
+//    kernel (D, dQ) recomputes S and dP instead (no T^2 memory).
 //  * causal blocks above the diagonal are skipped per wave; blocks are
 //    launched heaviest first.
 //  * head dims up to 64 (multiple of 4); smaller heads are zero-padded to 32.
@@ -357,11 +363,41 @@ __global__ void __launch_bounds__(256, 2) attn_bwd_dq_kernel(
   store_T_tile<HDP>(stage, dq, sm_scale, dqbase, rs, qw0, sh.T, sh.hd, lane);
 }
 
+// ------------------------------------------------ backward: D = rowsum(dO o O)
+// One block per token row (b, t) at a time: the block reads the row's H hd
+// floats of dO and O once, coalesced, stores the float4 partial dots in LDS
+// (C / 4 floats of dynamic shared memory) and thread h adds up head h's
+// hd / 4 partials in order.  D laid out [B, H, T].
+__global__ void __launch_bounds__(256) attn_bwd_d_kernel(const float* __restrict__ dout,
+                                                         const float* __restrict__ out,
+                                                         float* __restrict__ D, int B, int T, int H,
+                                                         int hd) {
+  extern __shared__ float part[];
+  const int C4 = H * hd / 4, hq = hd / 4;
+  const long long rows = (long long)B * T;
+  for (long long row = blockIdx.x; row < rows; row += gridDim.x) {
+    const floatx4* g = reinterpret_cast<const floatx4*>(dout + row * H * hd);
+    const floatx4* o = reinterpret_cast<const floatx4*>(out + row * H * hd);
+    for (int i = threadIdx.x; i < C4; i += 256) {
+      const floatx4 a = g[i], c = o[i];
+      part[i] = (a[0] * c[0] + a[1] * c[1]) + (a[2] * c[2] + a[3] * c[3]);
+    }
+    __syncthreads();
+    const int b = (int)(row / T), t = (int)(row % T);
+    for (int h = threadIdx.x; h < H; h += 256) {
+      float acc = 0.f;
+      for (int j = 0; j < hq; ++j) acc += part[h * hq + j];
+      D[((long long)b * H + h) * T + t] = acc;
+    }
+    __syncthreads();
+  }
+}
+
 // ------------------------------------------------ backward: dK and dV (key-major)
 template <int HDP>
 __global__ void __launch_bounds__(256, 1) attn_bwd_dkv_kernel(
     const float* __restrict__ dout, const float* __restrict__ qkv, const float* __restrict__ lse,
-    const float* __restrict__ Dws, float* __restrict__ dqkv, AttnShape sh) {
+    const float* __restrict__ Dws, float* __restrict__ dqkv, float* __restrict__ dS, AttnShape sh) {
   constexpr int LD = HDP + 4;
   constexpr int TSZ = 32 * LD;
   // per buffer: Q tile, dO tile, lse2[32], D[32]
@@ -387,6 +423,9 @@ __global__ void __launch_bounds__(256, 1) attn_bwd_dkv_kernel(
   const int kw0 = k0 + 32 * wave;
   const int my_k = kw0 + lr;
   const float sm_scale = 1.f / sqrtf((float)sh.hd);
+  // dS / sqrt(hd) for the dQ product, [B, H, T, T], column my_k of this lane
+  float* ds_col = dS ? dS + (long long)bh * sh.T * sh.T + my_k : nullptr;
+  const bool ds_lane = my_k < sh.T;
 
   float kf[HDP / 2], vf[HDP / 2];
   load_reg_operand<HDP>(kf, kbase, rs, my_k, sh.T, sh.hd, hh, LOG2E * sm_scale);
@@ -454,6 +493,23 @@ __global__ void __launch_bounds__(256, 1) attn_bwd_dkv_kernel(
       }
       mma_tile_T_by_acc<HDP, LD>(dv, sdO, s, lr, hh);  // dV^T[d][key] += dO^T P
       mma_tile_T_by_acc<HDP, LD>(dk, sQ, dp, lr, hh);  // dK^T[d][key] += Q^T dS
+      if (ds_col && ds_lane) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int q = qv0 + acc_row(r, hh);
+          if (q < sh.T) ds_col[(long long)q * sh.T] = dp[r] * sm_scale;
+        }
+      }
+    } else if (ds_col && ds_lane && qb < my_first) {
+      // query blocks of the diagonal 128-row tile that precede this wave's
+      // keys: fully masked, stored as zeros because the dQ product of that
+      // tile sums keys up to the tile's end
+      const int qv0 = qb * 32;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int q = qv0 + acc_row(r, hh);
+        if (q < sh.T) ds_col[(long long)q * sh.T] = 0.f;
+      }
     }
     if (more) store_q(smem + (cur ^ 1) * BUF);
     __syncthreads();
@@ -494,10 +550,20 @@ extern "C" bt_status bt_attention_fwd(const float* qkv, float* out, float* lse, 
   return check_launch("attn_fwd_kernel");
 }
 
-extern "C" size_t bt_attention_bwd_ws_bytes(int B, int T, int H, int hd) {
+extern "C" size_t bt_attention_bwd_ws_min_bytes(int B, int T, int H, int hd) {
   (void)hd;
   if (B <= 0 || T <= 0 || H <= 0) return 0;
   return align_up((size_t)B * H * T * sizeof(float), 256);
+}
+
+// The stored-dS backward reads dS rows as float4 along the keys: T % 4 == 0.
+bool attn_stores_ds(int T) { return T % 4 == 0; }
+
+extern "C" size_t bt_attention_bwd_ws_bytes(int B, int T, int H, int hd) {
+  if (B <= 0 || T <= 0 || H <= 0) return 0;
+  const size_t base = bt_attention_bwd_ws_min_bytes(B, T, H, hd);
+  if (!attn_stores_ds(T)) return base;
+  return base + align_up((size_t)B * H * T * T * sizeof(float), 256);
 }
 
 extern "C" bt_status bt_attention_bwd(const float* dout, const float* qkv, const float* out,
@@ -508,21 +574,42 @@ extern "C" bt_status bt_attention_bwd(const float* dout, const float* qkv, const
   BT_RETURN_IF(!aligned16(qkv) || !aligned16(out) || !aligned16(dout) || !aligned16(dqkv), BT_EALIGN,
                "bt_attention_bwd: tensors must be 16-byte aligned");
   BT_RETURN_IF(dqkv == qkv, BT_EINVAL, "bt_attention_bwd: dqkv must not alias qkv");
-  const size_t need = bt_attention_bwd_ws_bytes(B, T, H, hd);
-  BT_RETURN_IF(!ws || ws_bytes < need, BT_EWORKSPACE, "bt_attention_bwd: workspace of %zu bytes needed (got %zu)",
-               need, ws_bytes);
+  const size_t need_min = bt_attention_bwd_ws_min_bytes(B, T, H, hd);
+  BT_RETURN_IF(!ws || ws_bytes < need_min, BT_EWORKSPACE,
+               "bt_attention_bwd: workspace of %zu bytes needed (got %zu)", need_min, ws_bytes);
+  BT_RETURN_IF(!aligned16(ws), BT_EALIGN, "bt_attention_bwd: workspace must be 16-byte aligned");
   AttnShape sh{B, T, H, hd, 3LL * H * hd};
   float* D = static_cast<float*>(ws);
   dim3 gq((unsigned)(B * H * ((T + 127) / 128)));
   hipStream_t s = as_stream(stream);
+  if (attn_stores_ds(T) && ws_bytes >= bt_attention_bwd_ws_bytes(B, T, H, hd)) {
+    // D, then dK/dV with dS stored, then dQ = dS K (scale folded into dS)
+    float* dS = reinterpret_cast<float*>(static_cast<char*>(ws) + need_min);
+    const long long rows = (long long)B * T;
+    const unsigned gd = (unsigned)(rows < 8192 ? rows : 8192);
+    const size_t part_bytes = (size_t)H * hd / 4 * sizeof(float);
+    BT_RETURN_IF(part_bytes > 64 * 1024, BT_ESHAPE, "bt_attention_bwd: H * hd = %d too large", H * hd);
+    hipLaunchKernelGGL(attn_bwd_d_kernel, dim3(gd), dim3(256), part_bytes, s, dout, out, D, B, T, H, hd);
+    BT_TRY(check_launch("attn_bwd_d_kernel"));
+    if (hd <= 32)
+      hipLaunchKernelGGL(attn_bwd_dkv_kernel<32>, gq, dim3(256), 0, s, dout, qkv, lse, D, dqkv, dS, sh);
+    else
+      hipLaunchKernelGGL(attn_bwd_dkv_kernel<64>, gq, dim3(256), 0, s, dout, qkv, lse, D, dqkv, dS, sh);
+    BT_TRY(check_launch("attn_bwd_dkv_kernel"));
+    const long long rs = sh.row_stride;
+    // per (b, h): dQ [T][hd] (rows of dqkv, stride 3 H hd) = dS [T][T] K [T][hd]
+    return gemm_causal_batched(T, hd, T, dS, T, (long long)H * T * T, (long long)T * T,
+                               qkv + (long long)H * hd, (int)rs, (long long)T * rs, hd,
+                               dqkv, (int)rs, (long long)T * rs, hd, B, H, s);
+  }
   if (hd <= 32) {
     hipLaunchKernelGGL(attn_bwd_dq_kernel<32>, gq, dim3(256), 0, s, dout, qkv, out, lse, dqkv, D, sh);
     BT_TRY(check_launch("attn_bwd_dq_kernel"));
-    hipLaunchKernelGGL(attn_bwd_dkv_kernel<32>, gq, dim3(256), 0, s, dout, qkv, lse, D, dqkv, sh);
+    hipLaunchKernelGGL(attn_bwd_dkv_kernel<32>, gq, dim3(256), 0, s, dout, qkv, lse, D, dqkv, nullptr, sh);
   } else {
     hipLaunchKernelGGL(attn_bwd_dq_kernel<64>, gq, dim3(256), 0, s, dout, qkv, out, lse, dqkv, D, sh);
     BT_TRY(check_launch("attn_bwd_dq_kernel"));
-    hipLaunchKernelGGL(attn_bwd_dkv_kernel<64>, gq, dim3(256), 0, s, dout, qkv, lse, D, dqkv, sh);
+    hipLaunchKernelGGL(attn_bwd_dkv_kernel<64>, gq, dim3(256), 0, s, dout, qkv, lse, D, dqkv, nullptr, sh);
   }
   return check_launch("attn_bwd_dkv_kernel");
 }

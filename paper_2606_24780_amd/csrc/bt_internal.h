@@ -35,6 +35,14 @@ bt_status fill_zero(float* p, size_t n, hipStream_t s);
 bt_status sum_partials(const float* part, int nb, long long ld, int n, float* out_a, int n_a, float* out_b,
                        float beta, hipStream_t s);
 
+// Batch of products C_y = A_y B_y (A [M][K] row-major, B [K][N] row-major),
+// batch y < nb nh at A + (y / nh) sa_b + (y % nh) sa_h (likewise B, C), in
+// which output rows of each 128-row tile starting at m0 sum only k < m0 + 128
+// (exact when A_y[m][k] = 0 for k > m, e.g. causal attention scores).
+bt_status gemm_causal_batched(int M, int N, int K, const float* A, int lda, long long sa_b, long long sa_h,
+                              const float* B, int ldb, long long sb_b, long long sb_h, float* C, int ldc,
+                              long long sc_b, long long sc_h, int nb, int nh, hipStream_t stream);
+
 // ------------------------------------------------------------------ device
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));

@@ -67,6 +67,10 @@ struct GemmParams {
   int splits;
   int tiles_m, tiles_n;
   float beta;
+  // batched causal products only: batch y addresses A + (y / batch_h) sa_b +
+  // (y % batch_h) sa_h (likewise B, C)
+  int nbatch, batch_h;
+  long long sa_b, sa_h, sb_b, sb_h, sc_b, sc_h;
 };
 
 // LDS floats of one R-row operand tile: K-contiguous [R][BK] (swizzled) or
@@ -271,8 +275,15 @@ __device__ __forceinline__ void epilogue_block(const GemmParams& p, const floatx
 // full (M, N multiples of the block tile, K range a multiple of BK), and
 // operand tiles are copied straight from global memory into LDS; otherwise
 // they are staged through registers with bounds checks (ragged shapes).
-template <bool A_KC, bool B_KC, int EPI, bool SPLIT, bool COLSUM, int BK, int OCC, int WM, int WN, bool DTL>
-__global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmParams p) {
+// CAUSAL: a batch of products (blockIdx.x % nbatch selects the batch) in
+// which the output rows of a tile starting at m0 only sum k < m0 + BM; tile
+// rows are launched heaviest first.  OCC is the number of waves per SIMD the
+// register allocation must allow (the second launch-bounds argument on
+// AMDGPU); a CU then holds 4 OCC / (WM WN) blocks.
+template <bool A_KC, bool B_KC, int EPI, bool SPLIT, bool COLSUM, int BK, int OCC, int WM, int WN, bool DTL,
+          bool CAUSAL>
+__global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmParams pk) {
+  GemmParams p = pk;
   constexpr int BM = 64 * WM, BN = 64 * WN, NW = WM * WN, NT = 64 * NW;
   constexpr int A_SZ = TileSize<A_KC, BM, BK, DTL>::value;
   constexpr int B_SZ = TileSize<B_KC, BN, BK, DTL>::value;
@@ -284,7 +295,7 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
                 "direct copies must tile the operand tiles in 1 KB slices");
   static_assert(!DTL || (BM <= 256 && BN <= 256), "an MN-contiguous k-row must fit one wave copy");
   static_assert(DTL || !COLSUM || 4 * NT <= 2 * (A_SZ + B_SZ), "column-sum combine needs 16 B per thread of LDS");
-  static_assert(2 * (A_SZ + B_SZ) * 4 * OCC <= 160 * 1024, "LDS exceeds one CU at this occupancy");
+  static_assert(2 * (A_SZ + B_SZ) * 4 * (4 * OCC / NW) <= 160 * 1024, "LDS exceeds one CU at this occupancy");
   __shared__ __attribute__((aligned(16))) float smem[2 * (A_SZ + B_SZ)];
 
   const int tid = threadIdx.x;
@@ -294,24 +305,38 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
   const int hh = lane >> 5;
   const int wm = wave / WN, wn = wave % WN;
 
-  // ---- tile scheduling: XCD-contiguous ranges of a grouped tile order
-  const int ntiles = p.tiles_m * p.tiles_n;
-  const int total = gridDim.x;
-  int bid = blockIdx.x;
-  if ((total & 7) == 0) bid = (bid & 7) * (total >> 3) + (bid >> 3);
-  const int z = bid / ntiles;
-  const int tile = bid - z * ntiles;
-  const int group = 8 * p.tiles_n;
-  const int gid = tile / group;
-  const int first_m = gid * 8;
-  const int gsz = min(p.tiles_m - first_m, 8);
-  const int in_g = tile - gid * group;
-  const int tm = first_m + in_g % gsz;
-  const int tn = in_g / gsz;
+  int z, tm, tn;
+  if (CAUSAL) {
+    const int y = blockIdx.x % p.nbatch;
+    const int rank = blockIdx.x / p.nbatch;  // 0: last tile row (longest k range)
+    tm = p.tiles_m - 1 - rank / p.tiles_n;
+    tn = rank % p.tiles_n;
+    z = 0;
+    const int yb = y / p.batch_h, yh = y % p.batch_h;
+    p.A += yb * p.sa_b + yh * p.sa_h;
+    p.B += yb * p.sb_b + yh * p.sb_h;
+    p.C += yb * p.sc_b + yh * p.sc_h;
+  } else {
+    // ---- tile scheduling: XCD-contiguous ranges of a grouped tile order
+    const int ntiles = p.tiles_m * p.tiles_n;
+    const int total = gridDim.x;
+    int bid = blockIdx.x;
+    if ((total & 7) == 0) bid = (bid & 7) * (total >> 3) + (bid >> 3);
+    z = bid / ntiles;
+    const int tile = bid - z * ntiles;
+    const int group = 8 * p.tiles_n;
+    const int gid = tile / group;
+    const int first_m = gid * 8;
+    const int gsz = min(p.tiles_m - first_m, 8);
+    const int in_g = tile - gid * group;
+    tm = first_m + in_g % gsz;
+    tn = in_g / gsz;
+  }
   const int m0 = tm * BM, n0 = tn * BN;
 
   const int kbeg = z * p.ksplit;
-  const int kend = min(p.K, kbeg + p.ksplit);
+  int kend = min(p.K, kbeg + p.ksplit);
+  if (CAUSAL) kend = min(kend, m0 + BM);
   const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
 
   floatx16 acc[2][2];
@@ -507,7 +532,8 @@ __global__ void __launch_bounds__(256) splitk_colsum_reduce(const float* __restr
 }
 
 // Block-tile configurations: tile depth, wave grid (64 x 64 outputs per
-// wave), resident blocks per CU, and the relative rate of one CU working
+// wave), resident blocks per CU (= waves per SIMD for 4-wave blocks), and
+// the relative rate of one CU working
 // through 128 x 128 x 16 tile steps when it holds its full complement of
 // blocks (K-contiguous operand present / both operands MN-contiguous),
 // measured on MI355X.  Larger block tiles (256 x 128, 128 x 256, 256 x 256)
@@ -576,26 +602,26 @@ void launch_cfg(const GemmParams& p, int epi, bool split, dim3 grid, hipStream_t
   const dim3 block(64 * WM * WN);
   if (split) {
     if (cs)
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, !B_KC, BK, OCC, WM, WN, DTL>), grid, block, 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, !B_KC, BK, OCC, WM, WN, DTL, false>), grid, block, 0, s, p);
     else
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, false, BK, OCC, WM, WN, DTL>), grid, block, 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, false, BK, OCC, WM, WN, DTL, false>), grid, block, 0, s, p);
     return;
   }
   switch (epi) {
     case BT_EPI_NONE:
       if (cs)
-        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, !B_KC, BK, OCC, WM, WN, DTL>), grid, block, 0, s, p);
+        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, !B_KC, BK, OCC, WM, WN, DTL, false>), grid, block, 0, s, p);
       else
-        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, false, BK, OCC, WM, WN, DTL>), grid, block, 0, s, p);
+        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, false, BK, OCC, WM, WN, DTL, false>), grid, block, 0, s, p);
       break;
     case BT_EPI_BIAS:
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS, false, false, BK, OCC, WM, WN, DTL>), grid, block, 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS, false, false, BK, OCC, WM, WN, DTL, false>), grid, block, 0, s, p);
       break;
     case BT_EPI_BIAS_GELU:
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS_GELU, false, false, BK, OCC, WM, WN, DTL>), grid, block, 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS_GELU, false, false, BK, OCC, WM, WN, DTL, false>), grid, block, 0, s, p);
       break;
     default:
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_DGELU, false, false, BK, OCC, WM, WN, DTL>), grid, block, 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_DGELU, false, false, BK, OCC, WM, WN, DTL, false>), grid, block, 0, s, p);
       break;
   }
 }
@@ -614,6 +640,52 @@ void launch_layout(const GemmParams& p, const GemmCfg& c, int epi, bool split, b
 }
 
 }  // namespace
+
+bt_status gemm_causal_batched(int M, int N, int K, const float* A, int lda, long long sa_b, long long sa_h,
+                              const float* B, int ldb, long long sb_b, long long sb_h, float* C, int ldc,
+                              long long sc_b, long long sc_h, int nb, int nh, hipStream_t stream) {
+  BT_RETURN_IF(M <= 0 || N <= 0 || K <= 0 || nb <= 0 || nh <= 0, BT_ESHAPE,
+               "gemm_causal_batched: bad sizes M=%d N=%d K=%d nb=%d nh=%d", M, N, K, nb, nh);
+  BT_RETURN_IF((M | N | K | lda | ldb | ldc) & 3, BT_ESHAPE, "gemm_causal_batched: sizes and strides must be multiples of 4");
+  BT_RETURN_IF(!aligned16(A) || !aligned16(B) || !aligned16(C) || ((sa_b | sa_h | sb_b | sb_h | sc_b | sc_h) & 3),
+               BT_EALIGN, "gemm_causal_batched: operands must be 16-byte aligned");
+  // 2 waves per SIMD: measured faster on MI355X than 3 (the tighter register
+  // budget of 3 costs more than the extra resident waves gain)
+  constexpr int WM = 2, WN = 1, BK = 16, OCC = 2;
+  GemmParams p{};
+  p.A = A;
+  p.B = B;
+  p.C = C;
+  p.lda = lda;
+  p.ldb = ldb;
+  p.ldc = ldc;
+  p.M = M;
+  p.N = N;
+  p.K = K;
+  p.ksplit = (K + BK - 1) / BK * BK;
+  p.splits = 1;
+  p.tiles_m = (M + 64 * WM - 1) / (64 * WM);
+  p.tiles_n = (N + 64 * WN - 1) / (64 * WN);
+  p.nbatch = nb * nh;
+  p.batch_h = nh;
+  p.sa_b = sa_b;
+  p.sa_h = sa_h;
+  p.sb_b = sb_b;
+  p.sb_h = sb_h;
+  p.sc_b = sc_b;
+  p.sc_h = sc_h;
+  const long long nblocks = (long long)p.tiles_m * p.tiles_n * p.nbatch;
+  BT_RETURN_IF(nblocks > 0x7fffffffLL, BT_ESHAPE, "gemm_causal_batched: too many tiles");
+  const bool dtl = M % (64 * WM) == 0 && N % (64 * WN) == 0 && K % BK == 0;
+  if (dtl)
+    hipLaunchKernelGGL((gemm_f32_mfma<true, false, BT_EPI_NONE, false, false, BK, OCC, WM, WN, true, true>),
+                       dim3((unsigned)nblocks), dim3(64 * WM * WN), 0, stream, p);
+  else
+    hipLaunchKernelGGL((gemm_f32_mfma<true, false, BT_EPI_NONE, false, false, BK, OCC, WM, WN, false, true>),
+                       dim3((unsigned)nblocks), dim3(64 * WM * WN), 0, stream, p);
+  return check_launch("gemm_f32_mfma (batched causal)");
+}
+
 }  // namespace bt
 
 using namespace bt;

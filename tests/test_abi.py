@@ -104,6 +104,22 @@ def test_other_validation(lib):
     assert lib.bt_grad_norm_clip(FAKE, 8, 1.0, None, None, None, 0, None) == BT_EINVAL
 
 
+def test_attention_workspace_sizes(lib):
+    """Row sums D always; the stored-dS method adds B H T T floats when T % 4 == 0."""
+    def al(x):
+        return (x + 255) // 256 * 256
+    for B, T, H in [(16, 1024, 12), (2, 256, 3), (2, 37, 2), (1, 1, 1)]:
+        small = lib.bt_attention_bwd_ws_min_bytes(B, T, H, 64)
+        full = lib.bt_attention_bwd_ws_bytes(B, T, H, 64)
+        assert small == al(4 * B * H * T)
+        assert full == (small + al(4 * B * H * T * T) if T % 4 == 0 else small)
+    assert lib.bt_attention_bwd_ws_bytes(0, 16, 1, 64) == 0
+    # below the minimum workspace the call is rejected before any launch
+    small = lib.bt_attention_bwd_ws_min_bytes(1, 16, 1, 64)
+    assert lib.bt_attention_bwd(FAKE, FAKE + 8192, FAKE, FAKE, FAKE + 16384, FAKE + 32768, small - 1,
+                                1, 16, 1, 64, None) == BT_EWORKSPACE
+
+
 def test_gpt2_context_validation(lib):
     cfg = bt.make_config(synth.TINY, synth.HP_TINY)
     need = lib.bt_gpt2_workspace_bytes(ctypes.byref(cfg), 2, 32)

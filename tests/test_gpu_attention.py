@@ -17,24 +17,29 @@ pytestmark = pytest.mark.gpu
 RNG = np.random.Generator(np.random.PCG64(3))
 
 
-def _run(torch, qkv, dout, B, T, H, hd):
+def _run(torch, qkv, dout, B, T, H, hd, small_ws=False):
     q = dev(torch, qkv.reshape(B * T, 3 * H * hd))
     out = torch.empty((B * T, H * hd), device="cuda")
     lse = torch.empty((B, H, T), device="cuda")
     bt.bt_attention_fwd(q, out, lse, B, T, H, hd)
     dq = torch.empty_like(q)
-    bt.bt_attention_bwd(dev(torch, dout.reshape(B * T, H * hd)), q, out, lse, dq, B, T, H, hd)
+    bt.bt_attention_bwd(dev(torch, dout.reshape(B * T, H * hd)), q, out, lse, dq, B, T, H, hd,
+                        small_ws=small_ws)
     return (host(out).reshape(B, T, H, hd), host(lse), host(dq).reshape(B, T, 3, H, hd))
 
 
+# small_ws=False stores dS and forms dQ as a batched product (T % 4 == 0;
+# other T fall back to recomputation); small_ws=True always recomputes.
+@pytest.mark.parametrize("small_ws", [False, True])
 @pytest.mark.parametrize("B,T,H,hd", [(2, 37, 2, 16), (1, 128, 2, 64), (2, 200, 3, 64), (1, 1, 1, 64),
-                                      (3, 64, 4, 32), (1, 300, 1, 64), (2, 33, 2, 48)])
-def test_attention_small(B, T, H, hd):
+                                      (3, 64, 4, 32), (1, 300, 1, 64), (2, 33, 2, 48), (2, 256, 2, 64),
+                                      (1, 132, 2, 36)])
+def test_attention_small(B, T, H, hd, small_ws):
     torch = torch_gpu()
-    say(f"attention B={B} T={T} H={H} hd={hd}")
+    say(f"attention B={B} T={T} H={H} hd={hd} small_ws={small_ws}")
     qkv = RNG.standard_normal((B, T, 3, H, hd)).astype(np.float32)
     dout = RNG.standard_normal((B, T, H, hd)).astype(np.float32)
-    out, lse, dqkv = _run(torch, qkv, dout, B, T, H, hd)
+    out, lse, dqkv = _run(torch, qkv, dout, B, T, H, hd, small_ws)
     r_out, r_lse = ops.attention_fwd(qkv, H)
     r_dqkv = ops.attention_bwd(dout, qkv, H)
     assert_close_maxabs(out, r_out, 1e-5, "out")
@@ -70,6 +75,22 @@ def test_attention_deterministic():
     b = _run(torch, qkv, dout, B, T, H, hd)
     for x, y in zip(a, b):
         assert np.array_equal(x, y)
+
+
+def test_attention_bwd_methods_agree():
+    """Both backward methods share the key-major pass: dV (independent of
+    the row sums D) is bitwise equal; dK (D is summed in another order) and
+    dQ (stored dS times K vs recomputation) agree to rounding."""
+    torch = torch_gpu()
+    B, T, H, hd = 2, 256, 3, 64
+    qkv = RNG.standard_normal((B, T, 3, H, hd)).astype(np.float32)
+    dout = RNG.standard_normal((B, T, H, hd)).astype(np.float32)
+    say("attention backward methods agree")
+    _, _, d_big = _run(torch, qkv, dout, B, T, H, hd, small_ws=False)
+    _, _, d_small = _run(torch, qkv, dout, B, T, H, hd, small_ws=True)
+    assert np.array_equal(d_big[:, :, 2], d_small[:, :, 2])
+    assert_close_maxabs(d_big[:, :, 1], d_small[:, :, 1].astype(np.float64), 1e-5, "dK methods")
+    assert_close_maxabs(d_big[:, :, 0], d_small[:, :, 0].astype(np.float64), 1e-5, "dQ methods")
 
 
 def test_attention_gpt2_124m_sampled():
