@@ -270,8 +270,8 @@ __device__ __forceinline__ void epilogue_block(const GemmParams& p, const floatx
   }
 }
 
-// WM x WN waves, each owning a 64 x 64 output sub-tile: block tile
-// (64 WM) x (64 WN), 64 WM WN threads.  DTL: every tile of the launch is
+// WM x WN waves, each owning a (32 MB) x (32 NB) output sub-tile of MB x NB
+// MFMA accumulators: block tile (32 MB WM) x (32 NB WN), 64 WM WN threads.  DTL: every tile of the launch is
 // full (M, N multiples of the block tile, K range a multiple of BK), and
 // operand tiles are copied straight from global memory into LDS; otherwise
 // they are staged through registers with bounds checks (ragged shapes).
@@ -280,15 +280,16 @@ __device__ __forceinline__ void epilogue_block(const GemmParams& p, const floatx
 // rows are launched heaviest first.  OCC is the number of waves per SIMD the
 // register allocation must allow (the second launch-bounds argument on
 // AMDGPU); a CU then holds 4 OCC / (WM WN) blocks.
-template <bool A_KC, bool B_KC, int EPI, bool SPLIT, bool COLSUM, int BK, int OCC, int WM, int WN, bool DTL,
-          bool CAUSAL>
+template <bool A_KC, bool B_KC, int EPI, bool SPLIT, bool COLSUM, int BK, int OCC, int WM, int WN, int MB, int NB,
+          bool DTL, bool CAUSAL>
 __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmParams pk) {
   GemmParams p = pk;
-  constexpr int BM = 64 * WM, BN = 64 * WN, NW = WM * WN, NT = 64 * NW;
+  constexpr int WTM = 32 * MB, WTN = 32 * NB;  // wave tile: MB x NB MFMA 32x32 blocks
+  constexpr int BM = WTM * WM, BN = WTN * WN, NW = WM * WN, NT = 64 * NW;
   constexpr int A_SZ = TileSize<A_KC, BM, BK, DTL>::value;
   constexpr int B_SZ = TileSize<B_KC, BN, BK, DTL>::value;
-  constexpr int NA = DTL ? 1 : TileVecs<BM, BK, NT>::value;  // float4 staged per thread, A
-  constexpr int NB = DTL ? 1 : TileVecs<BN, BK, NT>::value;  // float4 staged per thread, B
+  constexpr int NVA = DTL ? 1 : TileVecs<BM, BK, NT>::value;  // float4 staged per thread, A
+  constexpr int NVB = DTL ? 1 : TileVecs<BN, BK, NT>::value;  // float4 staged per thread, B
   constexpr int CA = BM * BK / (256 * NW);  // direct 1 KB copies per wave per tile, A
   constexpr int CB = BN * BK / (256 * NW);  // direct 1 KB copies per wave per tile, B
   static_assert(!DTL || (CA >= 1 && CB >= 1 && CA * 256 * NW == BM * BK && CB * 256 * NW == BN * BK),
@@ -339,15 +340,15 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
   if (CAUSAL) kend = min(kend, m0 + BM);
   const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
 
-  floatx16 acc[2][2];
+  floatx16 acc[MB][NB];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < MB; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < NB; ++b)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
-  floatx4 ra[NA], rb[NB];
+  floatx4 ra[NVA], rb[NVB];
   const float* ga[CA];
   const float* gb[CB];
   const long long a_step = A_KC ? BK : (long long)BK * p.lda;  // per k-tile source advance
@@ -359,7 +360,9 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
   // reads (its column, its half of every k-tile) and the lane halves are
   // combined at the end.
   floatx4 csum = floatx4{0.f, 0.f, 0.f, 0.f};
-  floatx4 csf[2] = {floatx4{0.f, 0.f, 0.f, 0.f}, floatx4{0.f, 0.f, 0.f, 0.f}};
+  floatx4 csf[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) csf[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
   if (DTL) {
     copy_setup<A_KC, BM, BK, CA>(ga, p.A, p.lda, m0, kbeg, wave, lane);
     copy_setup<B_KC, BN, BK, CB>(gb, p.B, p.ldb, n0, kbeg, wave, lane);
@@ -374,7 +377,7 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
       load_tile<B_KC, BN, BK, NT>(rb, p.B, p.ldb, n0, p.N, kbeg, kend, tid);
       if (COLSUM)
 #pragma unroll
-        for (int i = 0; i < NB; ++i) csum += rb[i];
+        for (int i = 0; i < NVB; ++i) csum += rb[i];
       store_tile<A_KC, BM, BK, NT>(smem, ra, tid);
       store_tile<B_KC, BN, BK, NT>(smem + A_SZ, rb, tid);
     }
@@ -405,22 +408,22 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
 #pragma unroll
     for (int c = 0; c < BK / 8; ++c) {
       const int koff = 8 * hh + 4 * (c & 1) + 16 * (c >> 1);
-      floatx4 fa[2], fb[2];
+      floatx4 fa[MB], fb[NB];
 #pragma unroll
-      for (int mb = 0; mb < 2; ++mb) fa[mb] = read_frag<A_KC, BM, BK, DTL>(sA, wm * 64 + mb * 32 + lr, koff);
+      for (int mb = 0; mb < MB; ++mb) fa[mb] = read_frag<A_KC, BM, BK, DTL>(sA, wm * WTM + mb * 32 + lr, koff);
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb) fb[nb] = read_frag<B_KC, BN, BK, DTL>(sB, wn * 64 + nb * 32 + lr, koff);
+      for (int nb = 0; nb < NB; ++nb) fb[nb] = read_frag<B_KC, BN, BK, DTL>(sB, wn * WTN + nb * 32 + lr, koff);
 #pragma unroll
       for (int q = 0; q < 4; ++q)
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
+        for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-          for (int nb = 0; nb < 2; ++nb)
+          for (int nb = 0; nb < NB; ++nb)
             acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[mb][q], fb[nb][q], acc[mb][nb],
                                                                0, 0, 0);
       if (DTL && COLSUM) {
-        csf[0] += fb[0];
-        csf[1] += fb[1];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) csf[nb] += fb[nb];
       }
     }
     __builtin_amdgcn_s_setprio(0);
@@ -429,7 +432,7 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
     } else if (more) {
       if (COLSUM)
 #pragma unroll
-        for (int i = 0; i < NB; ++i) csum += rb[i];
+        for (int i = 0; i < NVB; ++i) csum += rb[i];
       float* sN = smem + (cur ^ 1) * (A_SZ + B_SZ);
       store_tile<A_KC, BM, BK, NT>(sN, ra, tid);
       store_tile<B_KC, BN, BK, NT>(sN + A_SZ, rb, tid);
@@ -442,10 +445,10 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
       // waves of the first wave row read every B column of the tile once
       if (wm == 0) {
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
+        for (int nb = 0; nb < NB; ++nb) {
           float v = (csf[nb][0] + csf[nb][1]) + (csf[nb][2] + csf[nb][3]);
           v += __shfl_xor(v, 32, 64);
-          const int n = n0 + wn * 64 + nb * 32 + lr;
+          const int n = n0 + wn * WTN + nb * 32 + lr;
           if (hh == 0 && n < p.N) {
             if (SPLIT) {
               p.ws_colsum[(long long)z * p.N + n] = v;
@@ -483,11 +486,11 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
   // ---- epilogue.  Accumulator element r of lane (lr, hh) of block (mb, nb):
   // row = 8 (r/4) + 4 hh + r%4, column = lr.
 #pragma unroll
-  for (int mb = 0; mb < 2; ++mb)
+  for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      const int j = n0 + wn * 64 + nb * 32 + lr;
-      const int i0 = m0 + wm * 64 + mb * 32;
+    for (int nb = 0; nb < NB; ++nb) {
+      const int j = n0 + wn * WTN + nb * 32 + lr;
+      const int i0 = m0 + wm * WTM + mb * 32;
       if (SPLIT) {
         if (j >= p.N) continue;
 #pragma unroll
@@ -536,15 +539,17 @@ __global__ void __launch_bounds__(256) splitk_colsum_reduce(const float* __restr
 // the relative rate of one CU working
 // through 128 x 128 x 16 tile steps when it holds its full complement of
 // blocks (K-contiguous operand present / both operands MN-contiguous),
-// measured on MI355X.  Larger block tiles (256 x 128, 128 x 256, 256 x 256)
-// were measured no faster on these shapes and are not offered.
+// measured on MI355X.  Larger block tiles (256 x 128, 128 x 256, 256 x 256
+// with 64 x 64 per wave) and larger wave tiles (64 x 128 or 128 x 64 at 2
+// waves per SIMD; 128 x 128 spills) were measured slower on most of the
+// model's shapes and are not offered.
 struct TileCfg {
-  int bk, wm, wn, occ;
+  int bk, wm, wn, mb, nb, occ;
   double rate_kc, rate_mn;
 };
 constexpr TileCfg kTileCfgs[] = {
-    {32, 2, 2, 2, 1.00, 1.00},
-    {16, 2, 2, 4, 1.0 / 0.95, 1.0 / 0.98},
+    {32, 2, 2, 2, 2, 2, 1.00, 1.00},
+    {16, 2, 2, 2, 2, 4, 1.0 / 0.95, 1.0 / 0.98},
 };
 constexpr int NUM_TILE_CFGS = (int)(sizeof(kTileCfgs) / sizeof(kTileCfgs[0]));
 
@@ -573,7 +578,7 @@ GemmCfg choose_config(int M, int N, int K, bool akc, bool bkc, bool may_split) {
   double best_t = 1e300;
   for (int tc = 0; tc < NUM_TILE_CFGS; ++tc) {
     const TileCfg& c = kTileCfgs[tc];
-    const int bm = 64 * c.wm, bn = 64 * c.wn, bk = c.bk;
+    const int bm = 32 * c.mb * c.wm, bn = 32 * c.nb * c.wn, bk = c.bk;
     const long long tiles = (long long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
     const int kt = (K + bk - 1) / bk;
     int smax = 1;
@@ -585,7 +590,7 @@ GemmCfg choose_config(int M, int N, int K, bool akc, bool bkc, bool may_split) {
       if (s > 1 && (double)s * M * N * sizeof(float) > (double)MAX_SPLIT_WS) continue;
       // time in 128 x 128 x 16 tile steps of a full CU
       const double work = (double)bm * bn / (128.0 * 128.0) * ks / 16.0 / ((akc || bkc) ? c.rate_kc : c.rate_mn);
-      double t = launch_time(tiles * s, c.occ, c.wm * c.wn, work);
+      double t = launch_time(tiles * s, c.occ * 4 / (c.wm * c.wn), c.wm * c.wn, work);
       if (s > 1) t += 4.0 * (double)s * M * N / (128.0 * 128.0) / NUM_CU;  // partial tiles out and back
       if (t < best_t * 0.995) {
         best_t = t;
@@ -596,32 +601,32 @@ GemmCfg choose_config(int M, int N, int K, bool akc, bool bkc, bool may_split) {
   return best;
 }
 
-template <bool A_KC, bool B_KC, int BK, int OCC, int WM, int WN, bool DTL>
+template <bool A_KC, bool B_KC, int BK, int OCC, int WM, int WN, int MB, int NB, bool DTL>
 void launch_cfg(const GemmParams& p, int epi, bool split, dim3 grid, hipStream_t s) {
   const bool cs = p.colsum != nullptr;
   const dim3 block(64 * WM * WN);
   if (split) {
     if (cs)
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, !B_KC, BK, OCC, WM, WN, DTL, false>), grid, block, 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, !B_KC, BK, OCC, WM, WN, MB, NB, DTL, false>), grid, block, 0, s, p);
     else
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, false, BK, OCC, WM, WN, DTL, false>), grid, block, 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, false, BK, OCC, WM, WN, MB, NB, DTL, false>), grid, block, 0, s, p);
     return;
   }
   switch (epi) {
     case BT_EPI_NONE:
       if (cs)
-        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, !B_KC, BK, OCC, WM, WN, DTL, false>), grid, block, 0, s, p);
+        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, !B_KC, BK, OCC, WM, WN, MB, NB, DTL, false>), grid, block, 0, s, p);
       else
-        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, false, BK, OCC, WM, WN, DTL, false>), grid, block, 0, s, p);
+        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, false, BK, OCC, WM, WN, MB, NB, DTL, false>), grid, block, 0, s, p);
       break;
     case BT_EPI_BIAS:
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS, false, false, BK, OCC, WM, WN, DTL, false>), grid, block, 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS, false, false, BK, OCC, WM, WN, MB, NB, DTL, false>), grid, block, 0, s, p);
       break;
     case BT_EPI_BIAS_GELU:
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS_GELU, false, false, BK, OCC, WM, WN, DTL, false>), grid, block, 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS_GELU, false, false, BK, OCC, WM, WN, MB, NB, DTL, false>), grid, block, 0, s, p);
       break;
     default:
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_DGELU, false, false, BK, OCC, WM, WN, DTL, false>), grid, block, 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_DGELU, false, false, BK, OCC, WM, WN, MB, NB, DTL, false>), grid, block, 0, s, p);
       break;
   }
 }
@@ -630,13 +635,14 @@ void launch_cfg(const GemmParams& p, int epi, bool split, dim3 grid, hipStream_t
 template <bool A_KC, bool B_KC>
 void launch_layout(const GemmParams& p, const GemmCfg& c, int epi, bool split, bool dtl, dim3 grid,
                    hipStream_t s) {
-  if (c.tc == 0) {
-    if (dtl) launch_cfg<A_KC, B_KC, 32, 2, 2, 2, true>(p, epi, split, grid, s);
-    else launch_cfg<A_KC, B_KC, 32, 2, 2, 2, false>(p, epi, split, grid, s);
-  } else {
-    if (dtl) launch_cfg<A_KC, B_KC, 16, 4, 2, 2, true>(p, epi, split, grid, s);
-    else launch_cfg<A_KC, B_KC, 16, 4, 2, 2, false>(p, epi, split, grid, s);
+#define BT_GEMM_CFG(BK_, OCC_, WM_, WN_, MB_, NB_)                                         \
+  if (dtl) launch_cfg<A_KC, B_KC, BK_, OCC_, WM_, WN_, MB_, NB_, true>(p, epi, split, grid, s); \
+  else launch_cfg<A_KC, B_KC, BK_, OCC_, WM_, WN_, MB_, NB_, false>(p, epi, split, grid, s)
+  switch (c.tc) {
+    case 0: BT_GEMM_CFG(32, 2, 2, 2, 2, 2); break;
+    default: BT_GEMM_CFG(16, 4, 2, 2, 2, 2); break;
   }
+#undef BT_GEMM_CFG
 }
 
 }  // namespace
@@ -678,10 +684,10 @@ bt_status gemm_causal_batched(int M, int N, int K, const float* A, int lda, long
   BT_RETURN_IF(nblocks > 0x7fffffffLL, BT_ESHAPE, "gemm_causal_batched: too many tiles");
   const bool dtl = M % (64 * WM) == 0 && N % (64 * WN) == 0 && K % BK == 0;
   if (dtl)
-    hipLaunchKernelGGL((gemm_f32_mfma<true, false, BT_EPI_NONE, false, false, BK, OCC, WM, WN, true, true>),
+    hipLaunchKernelGGL((gemm_f32_mfma<true, false, BT_EPI_NONE, false, false, BK, OCC, WM, WN, 2, 2, true, true>),
                        dim3((unsigned)nblocks), dim3(64 * WM * WN), 0, stream, p);
   else
-    hipLaunchKernelGGL((gemm_f32_mfma<true, false, BT_EPI_NONE, false, false, BK, OCC, WM, WN, false, true>),
+    hipLaunchKernelGGL((gemm_f32_mfma<true, false, BT_EPI_NONE, false, false, BK, OCC, WM, WN, 2, 2, false, true>),
                        dim3((unsigned)nblocks), dim3(64 * WM * WN), 0, stream, p);
   return check_launch("gemm_f32_mfma (batched causal)");
 }
@@ -748,7 +754,8 @@ extern "C" bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K, const fl
   const bool akc = opA == BT_OP_N;
   const bool bkc = opB == BT_OP_T;
   const GemmCfg cfg = choose_config(M, N, K, akc, bkc, may_split);
-  const int bm = 64 * kTileCfgs[cfg.tc].wm, bn = 64 * kTileCfgs[cfg.tc].wn;
+  const TileCfg& tcf = kTileCfgs[cfg.tc];
+  const int bm = 32 * tcf.mb * tcf.wm, bn = 32 * tcf.nb * tcf.wn;
   p.tiles_m = (M + bm - 1) / bm;
   p.tiles_n = (N + bn - 1) / bn;
   const int splits = cfg.splits;
