@@ -84,6 +84,25 @@ def calibrate_copy():
     print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n, "dispatches": 3}))
 
 
+def copy_bandwidth(torch, nbytes=1 << 30, reps=5):
+    """Achievable HBM bandwidth reference: a plain device-to-device copy of
+    nbytes (read + write counted), best of `reps` timed with HIP events."""
+    x = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    y.copy_(x)
+    best = float("inf")
+    for _ in range(reps):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        y.copy_(x)
+        e1.record()
+        torch.cuda.synchronize()
+        best = min(best, e0.elapsed_time(e1))
+    del x, y
+    return 2 * nbytes / (best / 1e3) / 1e9
+
+
 def cpu_baseline(sample_tokens: int):
     """The float64 oracle, as it stands, on a bounded sample of the same
     workload: one full step (fwd + bwd + clip + AdamW over all parameters)
@@ -163,6 +182,7 @@ def main():
     model.profile_enable(False)
 
     tok_s = a.steps * B * T / (ms / 1e3)
+    copy_gbs = copy_bandwidth(torch)
     g = prof["gemm"]
     gemm_tflops = g["flops"] / (g["ms"] / 1e3) / 1e12 if g["ms"] > 0 else 0.0
     kernels = {}
@@ -176,6 +196,7 @@ def main():
         if st["bytes"] > 0 and name not in ("gemm", "attn_fwd", "attn_bwd"):
             k["gbs"] = st["bytes"] / (st["ms"] / 1e3) / 1e9
             k["frac_hbm"] = k["gbs"] / HBM_PEAK_GBS
+            k["frac_copy"] = k["gbs"] / copy_gbs
         kernels[name] = k
     traffic, algo_bytes = gemm_traffic()
     roofline = {
@@ -201,6 +222,7 @@ def main():
         "wall_s": round(wall, 3),
         "loss_first_last": [losses[0], losses[-1]],
         "peak_mem_gib": round(torch.cuda.max_memory_allocated() / 2**30, 2),
+        "hbm_copy_gbs": round(copy_gbs, 1),
         "paper_context_tokens_s": PAPER_1GPU_TOKS,
     }
     if not a.no_cpu_baseline:
