@@ -181,6 +181,9 @@ struct Profiler {
   size_t used = 0;
   std::vector<ProfRec> pending;
   bt_kernel_stat stats[BT_PROF_NCLASSES] = {};
+  // end event of the previous profiled call when nothing has been enqueued
+  // on the stream since: the next call starts from it (one record per call)
+  hipEvent_t tail = nullptr;
 };
 
 }  // namespace
@@ -212,10 +215,16 @@ bt_status prof_flush(bt_gpt2_ctx* c) {
   }
   c->prof.pending.clear();
   c->prof.used = 0;
+  c->prof.tail = nullptr;
   return BT_OK;
 }
 
-// Brackets one library call with events when profiling is on.
+// Work not bracketed by a profiled call was (or may have been) enqueued: the
+// next profiled call records its own start event.
+void prof_break(bt_gpt2_ctx* c) { c->prof.tail = nullptr; }
+
+// Brackets one library call with events when profiling is on.  Back-to-back
+// calls share the event between them, so a step records one event per call.
 struct ProfScope {
   bt_gpt2_ctx* c;
   ProfRec rec;
@@ -225,12 +234,25 @@ struct ProfScope {
     if (c->prof.used + 2 > c->prof.pool.size()) {
       if (hipStreamSynchronize(c->stream) != hipSuccess || prof_flush(c) != BT_OK) return;
     }
-    rec = ProfRec{cls, flops, bytes, c->prof.pool[c->prof.used], c->prof.pool[c->prof.used + 1]};
-    c->prof.used += 2;
-    active = hipEventRecord(rec.a, c->stream) == hipSuccess;
+    rec = ProfRec{cls, flops, bytes, c->prof.tail, nullptr};
+    if (!rec.a) {
+      rec.a = c->prof.pool[c->prof.used++];
+      if (hipEventRecord(rec.a, c->stream) != hipSuccess) {
+        c->prof.tail = nullptr;
+        return;
+      }
+    }
+    rec.b = c->prof.pool[c->prof.used++];
+    active = true;
   }
   ~ProfScope() {
-    if (active && hipEventRecord(rec.b, c->stream) == hipSuccess) c->prof.pending.push_back(rec);
+    if (!active) return;
+    if (hipEventRecord(rec.b, c->stream) == hipSuccess) {
+      c->prof.pending.push_back(rec);
+      c->prof.tail = rec.b;
+    } else {
+      c->prof.tail = nullptr;
+    }
   }
 };
 
@@ -245,8 +267,13 @@ struct ProfScope {
 extern "C" bt_status bt_gpt2_profile_enable(bt_gpt2_ctx* ctx, int enable) {
   BT_RETURN_IF(!ctx, BT_EINVAL, "bt_gpt2_profile_enable: ctx is NULL");
   if (enable && ctx->prof.pool.empty()) {
-    ctx->prof.pool.resize(4096);
-    for (auto& e : ctx->prof.pool) BT_CHECK_HIP(hipEventCreate(&e));
+    // Timing-only events: without the system-scope fence an event record
+    // costs no cache writeback / invalidate (with it, ~4 us of GPU time per
+    // record, ~1.9 ms per GPT-2 124M step).  Elapsed times are read only
+    // after the stream has synchronised.  16384 events cover ~35 steps
+    // before the pool is flushed (a stream synchronisation).
+    ctx->prof.pool.resize(16384);
+    for (auto& e : ctx->prof.pool) BT_CHECK_HIP(hipEventCreateWithFlags(&e, hipEventDisableSystemFence));
   }
   ctx->prof.on = enable != 0;
   return BT_OK;
@@ -361,6 +388,7 @@ extern "C" bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, floa
   const bt_gpt2_config& cf = ctx->cfg;
   const ParamOffs& po = ctx->po;
   const Layout& ly = ctx->lay;
+  prof_break(ctx);  // the caller may have enqueued work since the last call
   StepBufs sb{ctx};
   hipStream_t s = ctx->stream;
   const int M = B * T, C = cf.C, F = 4 * cf.C, H = cf.H, hd = C / H, L = cf.L, Vp = cf.Vp;
@@ -418,7 +446,10 @@ extern "C" bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, floa
   // loss rows + dlogits = (softmax - onehot) * loss_scale, written over the logits
   BT_PROF(BT_PROF_XENT, 0, f4 * (2 * fM * fV + 3 * fM), bt_softmax_xent_fused(logits, targets, lrows, sb.f(ly.lse_rows), loss_scale, M, cf.V, Vp, s));
   BT_PROF(BT_PROF_OTHER, 0, f4 * fM, launch_loss_sum(lrows, M, loss_scale, accumulate, loss_dst, s));
-  if (loss_rows_out) BT_CHECK_HIP(hipMemcpyAsync(loss_rows_out, lrows, sizeof(float) * M, hipMemcpyDeviceToDevice, s));
+  if (loss_rows_out) {
+    prof_break(ctx);
+    BT_CHECK_HIP(hipMemcpyAsync(loss_rows_out, lrows, sizeof(float) * M, hipMemcpyDeviceToDevice, s));
+  }
 
   // ---------------- backward
   float* dres = sb.f(ly.dres);
@@ -469,7 +500,10 @@ extern "C" bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, floa
   }
   BT_PROF(BT_PROF_EMB_BWD, 0, f4 * (2 * fM * fC + 2 * (double)T * fC), bt_embedding_bwd(tokens, dres, G + po.wte, G + po.wpe, beta, scr, scrb, B, T, C, Vp, s));
   // rows of wpe beyond T receive no gradient in this micro-step
-  if (T < cf.max_T && !accumulate) BT_TRY(fill_zero(G + po.wpe + (size_t)T * C, (size_t)(cf.max_T - T) * C, s));
+  if (T < cf.max_T && !accumulate) {
+    prof_break(ctx);
+    BT_TRY(fill_zero(G + po.wpe + (size_t)T * C, (size_t)(cf.max_T - T) * C, s));
+  }
   return BT_OK;
 }
 
@@ -479,6 +513,7 @@ extern "C" bt_status bt_gpt2_optimizer_step(bt_gpt2_ctx* ctx, float* params, flo
   BT_RETURN_IF(t < 1, BT_EINVAL, "bt_gpt2_optimizer_step: t=%d must be >= 1", t);
   const bt_gpt2_config& cf = ctx->cfg;
   const size_t P = ctx->po.total;
+  prof_break(ctx);
   StepBufs sb{ctx};
   float* d_scal = sb.f(ctx->lay.scalars);
   const float* coef = nullptr;

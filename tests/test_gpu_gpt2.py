@@ -121,6 +121,46 @@ def test_tiny_step_deterministic():
     assert torch.equal(m1.opt_state, m2.opt_state)
 
 
+def test_step_profiler_counts_and_intervals():
+    """The step profiler (HIP events around every library call, the end of
+    one call shared with the start of the next): per-class call counts follow
+    the model's structure, GEMM flops are sum 2MNK, and the intervals add up to
+    no more than the steps' own event-timed duration (nothing counted twice)."""
+    torch = torch_gpu()
+    cfg, params, x, y = tiny_inputs()
+    B, T = x.shape
+    L, C, F, Vp = cfg.L, cfg.C, 4 * cfg.C, cfg.Vp
+    say("gpt2 tiny step profiler")
+    model = bt.GPT2(cfg, synth.HP_TINY, B, T)
+    model.load_params(synth.flatten(cfg, params))
+    xd, yd = dev(torch, x), dev(torch, y)
+    model.train_step(xd, yd)
+    model.profile_enable(True)
+    model.profile_read(reset=True)
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(model.stream)
+    steps = 2
+    for _ in range(steps):
+        model.train_step(xd, yd)
+    e1.record(model.stream)
+    torch.cuda.synchronize()
+    total_ms = e0.elapsed_time(e1)
+    prof = model.profile_read(reset=True)
+    model.profile_enable(False)
+    expect = {"gemm": 12 * L + 3, "attn_fwd": L, "attn_bwd": L, "ln_fwd": 2 * L + 1, "ln_bwd": 2 * L + 1,
+              "xent": 1, "emb_fwd": 1, "emb_bwd": 1, "grad_norm": 1, "adamw": 1}
+    for name, n in expect.items():
+        assert prof[name]["launches"] == steps * n, (name, prof[name]["launches"])
+        assert prof[name]["ms"] > 0, name
+    M = B * T
+    shapes = [(M, 3 * C, C), (M, C, C), (M, F, C), (M, C, F)]
+    flops = L * sum(2 * m * n * k * 3 for m, n, k in shapes) + 3 * 2 * M * Vp * C
+    assert prof["gemm"]["flops"] == pytest.approx(steps * flops, rel=1e-12)
+    assert sum(v["ms"] for v in prof.values()) <= total_ms * 1.001
+
+
 def test_tiny_multi_step_losses():
     torch = torch_gpu()
     cfg, params, x, y = tiny_inputs()
