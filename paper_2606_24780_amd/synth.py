@@ -72,6 +72,11 @@ class HParams:
 TINY = GPT2Config(V=256, Vp=256, max_T=32, L=2, H=4, C=64)
 # GPT-2 124M as in the hyper-parameter table.
 GPT2_124M = GPT2Config(V=50257, Vp=50304, max_T=1024, L=12, H=12, C=768)
+# Long-context single-GPU configuration (section "Long-context training"):
+# the 124M model with 16384 learned positions, run at B = 2, T = 16384.
+GPT2_124M_T16K = GPT2Config(V=50257, Vp=50304, max_T=16384, L=12, H=12, C=768)
+# Narrow model at long T whose whole step the float64 oracle can still run.
+TINY_T4K = GPT2Config(V=256, Vp=256, max_T=4096, L=2, H=4, C=64)
 
 HP_TINY = HParams(lr=3e-4, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.1, grad_clip=0.0)
 HP_124M = HParams(lr=6e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1, grad_clip=1.0)

@@ -1,0 +1,119 @@
+"""Long-context single-GPU step (section "Long-context training"): GPT-2 124M
+with 16384 learned positions at B = 2, T = 16384, and the kernels it leans on
+at long T.
+
+* attention at T = 4096 (2 heads) and T = 16384 (1 head) against the float64
+  oracle's full masked softmax, with both backward methods;
+* a narrow model (C = 64, L = 2, H = 4, V = 256) at T = 4096 through the whole
+  step (loss, every gradient, the AdamW update) against the oracle;
+* the 124M long-context model at B = 2, T = 16384: per-position losses of
+  positions < 2048 against the oracle run on the 2048-token prefix (position t
+  sees only tokens <= t, so the prefix computation is exact for them); the
+  same losses bitwise unchanged when every later token changes; a full train
+  step whose loss, gradients and updated parameters are finite."""
+import numpy as np
+import pytest
+
+from oracle import gpt2 as og
+from oracle import ops
+from paper_2606_24780_amd import bt, synth
+from tests.gpu_util import assert_close_maxabs, dev, host, say, torch_gpu
+from tests.test_gpu_gpt2 import GRAD_TOL, LOSS_TOL, _check_end_to_end, _check_update, _gpu_step, _unflat
+
+pytestmark = pytest.mark.gpu
+RNG = np.random.Generator(np.random.PCG64(16384))
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("B,T,H", [(1, 4096, 2), (1, 16384, 1)])
+def test_attention_long_T(B, T, H):
+    torch = torch_gpu()
+    hd = 64
+    qkv = RNG.standard_normal((B, T, 3, H, hd)).astype(np.float32)
+    dout = RNG.standard_normal((B, T, H, hd)).astype(np.float32)
+    say(f"attention long T: B={B} T={T} H={H}")
+    q = dev(torch, qkv.reshape(B * T, 3 * H * hd))
+    out = torch.empty((B * T, H * hd), device="cuda")
+    lse = torch.empty((B, H, T), device="cuda")
+    bt.bt_attention_fwd(q, out, lse, B, T, H, hd)
+    dqs = []
+    for small_ws in (False, True):
+        dq = torch.empty_like(q)
+        bt.bt_attention_bwd(dev(torch, dout.reshape(B * T, H * hd)), q, out, lse, dq, B, T, H, hd,
+                            small_ws=small_ws)
+        dqs.append(host(dq).reshape(B, T, 3, H, hd))
+    say("oracle attention (full masked softmax)")
+    r_out, r_lse = ops.attention_fwd(qkv, H)
+    assert_close_maxabs(host(out).reshape(B, T, H, hd), r_out, 1e-5, "out")
+    assert_close_maxabs(host(lse), r_lse, 1e-5, "lse")
+    r_d = ops.attention_bwd(dout, qkv, H)
+    for dq, how in zip(dqs, ("stored dS", "recompute")):
+        for i, n in enumerate("QKV"):
+            assert_close_maxabs(dq[:, :, i], r_d[:, :, i], 1e-4, f"d{n} ({how})")
+
+
+@pytest.mark.timeout(900)
+def test_narrow_model_T4096_step_vs_oracle():
+    torch = torch_gpu()
+    cfg, hp = synth.TINY_T4K, synth.HP_TINY
+    specs = synth.param_specs(cfg)
+    params = synth.init_params(cfg, 7)
+    B, T = 1, cfg.max_T
+    stream = synth.uniform_tokens(B * T + 1, cfg.V, np.random.Generator(np.random.PCG64(4097)))
+    x, y = synth.shifted_pair(stream, B, T)
+    say("narrow model T=4096 train step")
+    model, loss = _gpu_step(torch, cfg, hp, params, x, y)
+    zeros = {k: np.zeros_like(v, dtype=np.float64) for k, v in params.items()}
+    say("oracle train step")
+    ref = og.train_step(cfg, hp, specs, params, zeros, zeros, x, y, t=1)
+    say(f"loss gpu={loss:.8f} oracle={ref['loss']:.8f}")
+    assert abs(loss - ref["loss"]) <= LOSS_TOL * abs(ref["loss"])
+    g = _unflat(cfg, model.grads)
+    for name, _, _ in specs:
+        assert_close_maxabs(g[name], ref["grads"][name], GRAD_TOL, f"grad {name}")
+    p, m, v = _unflat(cfg, model.params), _unflat(cfg, model.m), _unflat(cfg, model.v)
+    _check_update(cfg, hp, specs, params, g, p, m, v, 1, what="T=4096")
+    _check_end_to_end(hp, specs, params, g, ref["grads"], p, ref["params"])
+
+
+@pytest.mark.timeout(900)
+def test_gpt2_124m_T16384_prefix_losses_causality_and_step():
+    torch = torch_gpu()
+    cfg, hp = synth.GPT2_124M_T16K, synth.HP_124M
+    B, T, P0 = 2, cfg.max_T, 2048
+    params = synth.init_params(cfg, 4)
+    stream = synth.zipf_tokens(B * T + 1, cfg.V, 1.1, 40)
+    x, y = synth.shifted_pair(stream, B, T)
+    say("gpt2 124M long context B=2 T=16384: forward loss rows")
+    model = bt.GPT2(cfg, hp, B, T)
+    model.load_params(synth.flatten(cfg, params))
+    d_loss = torch.zeros(1, device="cuda")
+    rows = torch.zeros(B * T, device="cuda")
+    model.fwd_bwd(dev(torch, x), dev(torch, y), 1.0 / (B * T), 0, d_loss, rows)
+    r1 = host(rows).reshape(B, T)
+    assert np.isfinite(r1).all()
+
+    say("same prefix, every later token changed")
+    x2, y2 = x.copy(), y.copy()
+    x2[:, P0:] = (x2[:, P0:] + 1 + RNG.integers(0, cfg.V - 1, size=x2[:, P0:].shape)) % cfg.V
+    y2[:, P0 - 1:] = (y2[:, P0 - 1:] + 7) % cfg.V
+    x2[:, :P0], y2[:, :P0 - 1] = x[:, :P0], y[:, :P0 - 1]
+    model.fwd_bwd(dev(torch, x2), dev(torch, y2), 1.0 / (B * T), 0, d_loss, rows)
+    r2 = host(rows).reshape(B, T)
+    assert np.array_equal(r1[:, :P0 - 1], r2[:, :P0 - 1])
+    assert not np.array_equal(r1[:, P0:], r2[:, P0:])
+
+    say(f"oracle forward of the {P0}-token prefix of sequence 0")
+    _, rr, _ = og.forward(cfg, params, x[0:1, :P0], y[0:1, :P0])
+    err = np.abs(r1[0, :P0] - rr).max() / np.abs(rr).max()
+    say(f"[parity] prefix loss rows: max rel {err:.3e}")
+    assert np.allclose(r1[0, :P0], rr, rtol=LOSS_TOL, atol=0)
+
+    say("full train step")
+    loss = model.train_step(dev(torch, x), dev(torch, y))
+    assert np.isfinite(loss)
+    assert abs(loss - r1.mean()) <= 1e-5 * r1.mean()
+    for t in (model.grads, model.params, model.opt_state):
+        assert bool(torch.isfinite(t).all())
+    wpe_g = host(model.grads)[synth.param_offsets(cfg)[1]:synth.param_offsets(cfg)[2]].reshape(cfg.max_T, cfg.C)
+    assert np.abs(wpe_g[T - 1]).max() > 0  # the last learned position receives a gradient
