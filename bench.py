@@ -1,11 +1,15 @@
 """Benchmark: GPT-2 124M FP32 training step on one MI355X.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--batch 16] [--no-cpu-baseline]
+    python bench.py --seq 16384            # long-context workload, B = 2
+    python bench.py --model 2.42b          # largest-trainable-model workload, B = 2
 
 One step = bt_gpt2_train_step: forward, backward, global-norm clip and AdamW
 over all 124,475,904 parameters, B x T = 16 x 1024 tokens of a seeded Zipf
 stream (a stand-in for the paper's FineWeb-Edu corpus), random-init weights
 of the paper's initialisation.  Inputs are resident in HBM before timing.
+The other two workloads print their own line (no CPU baseline: the float64
+oracle's full step does not fit a bounded sample there).
 
 Prints one JSON line: tokens/s over the K timed steps (HIP events on the
 library's stream, synchronised on both sides), the live roofline of the
@@ -27,6 +31,7 @@ MFMA_FP32_PEAK_TFLOPS = 157.3   # MI355X dense FP32 matrix peak
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E peak
 PAPER_1GPU_TOKS = 54600         # paper, 1 GPU eager (RTX 6000 Ada): context only
 PAPER_LONGCTX_TOKS = 17784      # paper, long-context table (RTX 6000 Ada, B=2, T=16384): context only
+PAPER_2B_TOKS = 13600           # paper, largest-model table (RTX 6000 Ada, 2.42B, B=2, T=1024): context only
 
 
 def parse():
@@ -34,7 +39,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--batch", type=int, default=16)
+    ap.add_argument("--model", choices=["124m", "2.42b"], default="124m",
+                    help="2.42b: the largest-trainable-model configuration (B = 2 by default)")
+    ap.add_argument("--batch", type=int, default=None, help="default 16 (124M, T <= 1024), else 2")
     ap.add_argument("--seq", type=int, default=1024)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=2048)
@@ -149,11 +156,16 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
-    B, T = a.batch, a.seq
-    long_ctx = T > synth.GPT2_124M.max_T
+    T = a.seq
+    big = a.model == "2.42b"
+    long_ctx = T > synth.GPT2_124M.max_T and not big
+    B = a.batch if a.batch is not None else (2 if big or long_ctx else 16)
     # T above 1024: the long-context configuration (the 124M model with T
     # learned positions; section "Long-context training" runs B = 2, T = 16384)
-    cfg = dataclasses.replace(synth.GPT2_124M, max_T=T) if long_ctx else synth.GPT2_124M
+    if big:
+        cfg = dataclasses.replace(synth.GPT2_2_42B, max_T=max(T, synth.GPT2_2_42B.max_T))
+    else:
+        cfg = dataclasses.replace(synth.GPT2_124M, max_T=T) if long_ctx else synth.GPT2_124M
     hp = synth.HP_124M
     params = synth.init_params(cfg, 4)
     stream = synth.zipf_tokens(B * T + 1, cfg.V, 1.1, 40)
@@ -215,12 +227,15 @@ def main():
         "flops_per_launch": g["flops"] / max(1, g["launches"]),
     }
     out = {
-        "metric": ("GPT-2 124M FP32 long-context train tokens/s on 1 GPU; GEMM fraction of FP32 MFMA peak"
+        "metric": ("GPT-2 2.42B FP32 train tokens/s on 1 GPU; GEMM fraction of FP32 MFMA peak" if big else
+                   "GPT-2 124M FP32 long-context train tokens/s on 1 GPU; GEMM fraction of FP32 MFMA peak"
                    if long_ctx else "GPT-2 124M FP32 train tokens/s on 1 GPU; GEMM fraction of FP32 MFMA peak"),
         "value": round(tok_s, 1), "unit": "tokens/s", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
         "ms_per_step": round(ms / a.steps, 3), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "f32", "data": "synthetic",
-        "config": {"workload": (f"GPT-2 124M FP32 long-context train step (fwd+bwd+clip+AdamW), {T} learned positions"
+        "config": {"workload": ("GPT-2 2.42B FP32 train step (fwd+bwd+clip+AdamW), largest-trainable-model configuration"
+                                if big else
+                                f"GPT-2 124M FP32 long-context train step (fwd+bwd+clip+AdamW), {T} learned positions"
                                 if long_ctx else
                                 "GPT-2 124M FP32 train step (fwd+bwd+clip+AdamW), one GPU's data-parallel shard"),
                    "batch": B, "seq_len": T, "layers": cfg.L, "d_model": cfg.C, "heads": cfg.H,
@@ -232,9 +247,9 @@ def main():
         "loss_first_last": [losses[0], losses[-1]],
         "peak_mem_gib": round(torch.cuda.max_memory_allocated() / 2**30, 2),
         "hbm_copy_gbs": round(copy_gbs, 1),
-        "paper_context_tokens_s": PAPER_LONGCTX_TOKS if long_ctx else PAPER_1GPU_TOKS,
+        "paper_context_tokens_s": PAPER_2B_TOKS if big else PAPER_LONGCTX_TOKS if long_ctx else PAPER_1GPU_TOKS,
     }
-    if not a.no_cpu_baseline:
+    if not a.no_cpu_baseline and not (big or long_ctx):
         out["cpu_baseline"] = cpu_baseline(a.cpu_sample_tokens)
     print(json.dumps(out))
 

@@ -104,8 +104,9 @@ size_t bt_gemm_ws_bytes(bt_op opA, bt_op opB, int M, int N, int K, bt_epi epi);
  *   qkv [B, T, 3, H, hd]   (the QKV projection output, [B*T, 3*H*hd])
  *   out [B, T, H, hd]      (written)
  *   lse [B, H, T]          (written; natural-log sum of exp of each score row)
- * hd a multiple of 4, at most 64 (heads below 32 are zero-padded to 32
- * inside the kernel).  T >= 1, B, H >= 1.  qkv and out 16-byte aligned.
+ * hd a multiple of 4, at most 128 (zero-padded to 32, 64 or 128 inside the
+ * kernels; 128 is the head dim of the 2.42B configuration).  T >= 1,
+ * B, H >= 1.  qkv and out 16-byte aligned.  Otherwise BT_ESHAPE / BT_EALIGN.
  */
 bt_status bt_attention_fwd(const float* qkv, float* out, float* lse,
                            int B, int T, int H, int hd, void* stream);

@@ -35,7 +35,9 @@
 //    kernel (D, dQ) recomputes S and dP instead (no T^2 memory).
 //  * causal blocks above the diagonal are skipped per wave; blocks are
 //    launched heaviest first.
-//  * head dims up to 64 (multiple of 4); smaller heads are zero-padded to 32.
+//  * head dims up to 128 (multiple of 4), zero-padded to 32, 64 or 128
+//    inside the kernels; at 128 the key-major backward keeps its dK/dV
+//    accumulators partly in AGPRs at one wave per SIMD.
 #include "bt_internal.h"
 
 namespace bt {
@@ -267,7 +269,7 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const float* __restric
 
 // ------------------------------------------------ backward: D and dQ (query-major)
 template <int HDP>
-__global__ void __launch_bounds__(256, 2) attn_bwd_dq_kernel(
+__global__ void __launch_bounds__(256, HDP > 64 ? 1 : 2) attn_bwd_dq_kernel(
     const float* __restrict__ dout, const float* __restrict__ qkv, const float* __restrict__ out,
     const float* __restrict__ lse, float* __restrict__ dqkv, float* __restrict__ Dws, AttnShape sh) {
   constexpr int LDK = HDP + 4;  // K: read as float4 (S) and as b32 (dQ)
@@ -523,8 +525,8 @@ __global__ void __launch_bounds__(256, 1) attn_bwd_dkv_kernel(
 
 bt_status check_attn(const void* a, const void* b2, int B, int T, int H, int hd, const char* who) {
   BT_RETURN_IF(B < 1 || T < 1 || H < 1, BT_ESHAPE, "%s: B=%d T=%d H=%d must be >= 1", who, B, T, H);
-  BT_RETURN_IF(hd < 4 || hd > 64 || (hd & 3), BT_ESHAPE,
-               "%s: head dim %d unsupported (multiple of 4, <= 64)", who, hd);
+  BT_RETURN_IF(hd < 4 || hd > 128 || (hd & 3), BT_ESHAPE,
+               "%s: head dim %d unsupported (multiple of 4, <= 128)", who, hd);
   BT_RETURN_IF(!a || !b2, BT_EINVAL, "%s: NULL pointer", who);
   BT_RETURN_IF((long long)B * H * ((T + 127) / 128) > 0x7fffffffLL, BT_ESHAPE, "%s: grid too large", who);
   return BT_OK;
@@ -545,8 +547,10 @@ extern "C" bt_status bt_attention_fwd(const float* qkv, float* out, float* lse, 
   hipStream_t s = as_stream(stream);
   if (hd <= 32)
     hipLaunchKernelGGL(attn_fwd_kernel<32>, grid, dim3(256), 0, s, qkv, out, lse, sh);
-  else
+  else if (hd <= 64)
     hipLaunchKernelGGL(attn_fwd_kernel<64>, grid, dim3(256), 0, s, qkv, out, lse, sh);
+  else
+    hipLaunchKernelGGL(attn_fwd_kernel<128>, grid, dim3(256), 0, s, qkv, out, lse, sh);
   return check_launch("attn_fwd_kernel");
 }
 
@@ -593,8 +597,10 @@ extern "C" bt_status bt_attention_bwd(const float* dout, const float* qkv, const
     BT_TRY(check_launch("attn_bwd_d_kernel"));
     if (hd <= 32)
       hipLaunchKernelGGL(attn_bwd_dkv_kernel<32>, gq, dim3(256), 0, s, dout, qkv, lse, D, dqkv, dS, sh);
-    else
+    else if (hd <= 64)
       hipLaunchKernelGGL(attn_bwd_dkv_kernel<64>, gq, dim3(256), 0, s, dout, qkv, lse, D, dqkv, dS, sh);
+    else
+      hipLaunchKernelGGL(attn_bwd_dkv_kernel<128>, gq, dim3(256), 0, s, dout, qkv, lse, D, dqkv, dS, sh);
     BT_TRY(check_launch("attn_bwd_dkv_kernel"));
     const long long rs = sh.row_stride;
     // per (b, h): dQ [T][hd] (rows of dqkv, stride 3 H hd) = dS [T][T] K [T][hd]
@@ -606,10 +612,14 @@ extern "C" bt_status bt_attention_bwd(const float* dout, const float* qkv, const
     hipLaunchKernelGGL(attn_bwd_dq_kernel<32>, gq, dim3(256), 0, s, dout, qkv, out, lse, dqkv, D, sh);
     BT_TRY(check_launch("attn_bwd_dq_kernel"));
     hipLaunchKernelGGL(attn_bwd_dkv_kernel<32>, gq, dim3(256), 0, s, dout, qkv, lse, D, dqkv, nullptr, sh);
-  } else {
+  } else if (hd <= 64) {
     hipLaunchKernelGGL(attn_bwd_dq_kernel<64>, gq, dim3(256), 0, s, dout, qkv, out, lse, dqkv, D, sh);
     BT_TRY(check_launch("attn_bwd_dq_kernel"));
     hipLaunchKernelGGL(attn_bwd_dkv_kernel<64>, gq, dim3(256), 0, s, dout, qkv, lse, D, dqkv, nullptr, sh);
+  } else {
+    hipLaunchKernelGGL(attn_bwd_dq_kernel<128>, gq, dim3(256), 0, s, dout, qkv, out, lse, dqkv, D, sh);
+    BT_TRY(check_launch("attn_bwd_dq_kernel"));
+    hipLaunchKernelGGL(attn_bwd_dkv_kernel<128>, gq, dim3(256), 0, s, dout, qkv, lse, D, dqkv, nullptr, sh);
   }
   return check_launch("attn_bwd_dkv_kernel");
 }

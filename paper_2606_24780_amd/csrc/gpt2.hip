@@ -75,7 +75,7 @@ bt_status check_config(const bt_gpt2_config* c) {
   BT_RETURN_IF(c->L < 1 || c->H < 1 || c->C < 4 || c->C % c->H || (c->C & 3), BT_ESHAPE,
                "gpt2: bad model shape L=%d H=%d C=%d", c->L, c->H, c->C);
   const int hd = c->C / c->H;
-  BT_RETURN_IF(hd > 64 || (hd & 3), BT_ESHAPE, "gpt2: head dim %d unsupported (multiple of 4, <= 64)", hd);
+  BT_RETURN_IF(hd > 128 || (hd & 3), BT_ESHAPE, "gpt2: head dim %d unsupported (multiple of 4, <= 128)", hd);
   BT_RETURN_IF(c->C > 4096, BT_ESHAPE, "gpt2: C=%d > 4096 unsupported", c->C);
   BT_RETURN_IF(c->V < 1 || c->Vp < c->V || (c->Vp & 3), BT_ESHAPE, "gpt2: V=%d Vp=%d (Vp >= V, multiple of 4)",
                c->V, c->Vp);

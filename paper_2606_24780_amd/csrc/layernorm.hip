@@ -210,9 +210,19 @@ __global__ void __launch_bounds__(64 * BWD_WAVES) ln_bwd_kernel(const float* dy,
 
 int ln_nv(int C) { return (C / 4 + 63) / 64; }
 
-int ln_bwd_blocks(int M) {
-  int nb = (M + 63) / 64;  // >= 64 rows per 16-wave block
-  if (nb > 256) nb = 256;  // one block per CU: few partials to combine
+// Waves per backward block for a row width (BwdWaves of the dispatched NV).
+int ln_bwd_waves(int C) {
+  const int nv = ln_nv(C);
+  return nv <= 2 ? 16 : (nv <= 4 ? 8 : 4);
+}
+
+// Backward blocks: about two rows per wave (a block of W waves takes >= 2W
+// rows), at most one block per CU so that few partial rows remain to be
+// combined.  Short inputs (M = 2048 rows of the 2.42B model) still spread
+// over every CU.
+int ln_bwd_blocks(int M, int waves) {
+  int nb = (M + 2 * waves - 1) / (2 * waves);
+  if (nb > 256) nb = 256;
   if (nb < 1) nb = 1;
   return nb;
 }
@@ -225,6 +235,7 @@ int ln_bwd_blocks(int M) {
     case 4: __VA_ARGS__(4); break;                     \
     case 5: case 6: __VA_ARGS__(6); break;             \
     case 7: case 8: __VA_ARGS__(8); break;             \
+    case 9: case 10: case 11: case 12: __VA_ARGS__(12); break; \
     default: __VA_ARGS__(16); break;                   \
   }
 
@@ -258,7 +269,7 @@ extern "C" bt_status bt_layernorm_fwd(const float* x, const float* gamma, const 
 
 extern "C" size_t bt_layernorm_bwd_ws_bytes(int M, int C) {
   if (M <= 0 || C <= 0) return 0;
-  return align_up((size_t)ln_bwd_blocks(M) * 2 * C * sizeof(float), 256);
+  return align_up((size_t)ln_bwd_blocks(M, ln_bwd_waves(C)) * 2 * C * sizeof(float), 256);
 }
 
 extern "C" bt_status bt_layernorm_bwd(const float* dy, const float* x, const float* gamma, const float* mean,
@@ -284,7 +295,7 @@ extern "C" bt_status bt_layernorm_bwd(const float* dy, const float* x, const flo
   const size_t need = bt_layernorm_bwd_ws_bytes(M, C);
   BT_RETURN_IF(!ws || ws_bytes < need, BT_EWORKSPACE, "bt_layernorm_bwd: workspace of %zu bytes needed (got %zu)",
                need, ws_bytes);
-  const int nb = ln_bwd_blocks(M);
+  const int nb = ln_bwd_blocks(M, ln_bwd_waves(C));
   const int rpb = (M + nb - 1) / nb;
   float* part = static_cast<float*>(ws);
 #define BT_LN_BWD(NV) hipLaunchKernelGGL(ln_bwd_kernel<NV>, dim3(nb), dim3(64 * BwdWaves<NV>::value), 0, s, dy, x, gamma, mean, rstd, dx, part, M, C, rpb, dx_beta)

@@ -77,6 +77,12 @@ GPT2_124M = GPT2Config(V=50257, Vp=50304, max_T=1024, L=12, H=12, C=768)
 GPT2_124M_T16K = GPT2Config(V=50257, Vp=50304, max_T=16384, L=12, H=12, C=768)
 # Narrow model at long T whose whole step the float64 oracle can still run.
 TINY_T4K = GPT2Config(V=256, Vp=256, max_T=4096, L=2, H=4, C=64)
+# Largest-trainable-model configuration (section "Largest trainable parameter
+# model"): 2.42B parameters, d_model 3072, 20 layers, 24 heads of dim 128,
+# run at B = 2, T = 1024.
+GPT2_2_42B = GPT2Config(V=50257, Vp=50304, max_T=1024, L=20, H=24, C=3072)
+# Narrow model with the 2.42B head dim (128), small enough for the oracle.
+TINY_HD128 = GPT2Config(V=256, Vp=256, max_T=64, L=2, H=2, C=256)
 
 HP_TINY = HParams(lr=3e-4, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.1, grad_clip=0.0)
 HP_124M = HParams(lr=6e-4, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1, grad_clip=1.0)

@@ -88,7 +88,7 @@ def test_gemm_validation(lib):
 
 
 def test_other_validation(lib):
-    assert lib.bt_attention_fwd(FAKE, FAKE, FAKE, 1, 16, 1, 128, None) == BT_ESHAPE
+    assert lib.bt_attention_fwd(FAKE, FAKE, FAKE, 1, 16, 1, 132, None) == BT_ESHAPE
     assert lib.bt_attention_fwd(FAKE, FAKE, FAKE, 0, 16, 1, 64, None) == BT_ESHAPE
     assert lib.bt_attention_bwd(FAKE, FAKE, FAKE, FAKE, FAKE + 4096, None, 0, 1, 16, 1, 64, None) == BT_EWORKSPACE
     assert lib.bt_attention_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20, 1, 16, 1, 64, None) == BT_EINVAL
@@ -128,8 +128,8 @@ def test_gpt2_context_validation(lib):
     assert lib.bt_gpt2_create(ctypes.byref(cfg), FAKE, need - 1, 2, 32, None, ctypes.byref(ctx)) == BT_EWORKSPACE
     assert lib.bt_gpt2_create(ctypes.byref(cfg), FAKE + 16, need, 2, 32, None, ctypes.byref(ctx)) == BT_EALIGN
     assert lib.bt_gpt2_create(ctypes.byref(cfg), FAKE, need, 2, 64, None, ctypes.byref(ctx)) == BT_ESHAPE
-    bad = bt.make_config(synth.GPT2Config(V=10, Vp=12, max_T=8, L=1, H=1, C=128), synth.HP_TINY)
-    assert lib.bt_gpt2_num_params(ctypes.byref(bad)) == 0  # head dim 128 unsupported
+    bad = bt.make_config(synth.GPT2Config(V=10, Vp=12, max_T=8, L=1, H=1, C=256), synth.HP_TINY)
+    assert lib.bt_gpt2_num_params(ctypes.byref(bad)) == 0  # head dim 256 unsupported
     assert lib.bt_gpt2_create(ctypes.byref(cfg), FAKE, need, 2, 32, None, ctypes.byref(ctx)) == BT_OK
     assert lib.bt_gpt2_step_count(ctx) == 0
     # a step larger than the context's token budget is rejected before any launch

@@ -33,7 +33,7 @@ def _run(torch, qkv, dout, B, T, H, hd, small_ws=False):
 @pytest.mark.parametrize("small_ws", [False, True])
 @pytest.mark.parametrize("B,T,H,hd", [(2, 37, 2, 16), (1, 128, 2, 64), (2, 200, 3, 64), (1, 1, 1, 64),
                                       (3, 64, 4, 32), (1, 300, 1, 64), (2, 33, 2, 48), (2, 256, 2, 64),
-                                      (1, 132, 2, 36)])
+                                      (1, 132, 2, 36), (2, 200, 2, 128), (1, 260, 2, 96), (1, 37, 1, 128)])
 def test_attention_small(B, T, H, hd, small_ws):
     torch = torch_gpu()
     say(f"attention B={B} T={T} H={H} hd={hd} small_ws={small_ws}")

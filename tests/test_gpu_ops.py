@@ -21,7 +21,8 @@ RNG = np.random.Generator(np.random.PCG64(4))
 
 
 # ------------------------------------------------------------------ LayerNorm
-@pytest.mark.parametrize("M,C", [(1, 64), (37, 768), (16384, 768), (5, 4096), (9, 1000)])
+@pytest.mark.parametrize("M,C", [(1, 64), (37, 768), (16384, 768), (5, 4096), (9, 1000), (2048, 3072),
+                                 (300, 2600)])
 def test_layernorm(M, C):
     torch = torch_gpu()
     say(f"layernorm M={M} C={C}")
