@@ -2,9 +2,9 @@
 // AdamW update over the flat parameter arena, the global gradient norm and
 // clip coefficient, column sums (bias gradients) and the loss reduction.
 //
-// All are single-pass, float4 (global_load_dwordx4), grid-stride with about
-// 8 blocks of 256 threads per CU in flight; reductions are two-stage with a
-// fixed order, so results are bitwise reproducible.
+// All are single-pass, float4 (global_load_dwordx4), grid-stride over up to
+// 128 blocks of 256 threads per CU; reductions are two-stage with a fixed
+// order, so results are bitwise reproducible.
 #include "bt_internal.h"
 
 namespace bt {
@@ -12,13 +12,21 @@ namespace {
 
 constexpr int EW_THREADS = 256;
 
-unsigned ew_blocks(size_t n4) {
+// Grid of the streaming kernels: up to 128 blocks per CU (256 CUs), each
+// thread a few grid-stride iterations.  Measured on MI355X over 124.5M
+// parameters: AdamW 4.67 TB/s at 8 blocks per CU, 5.31 TB/s at 128; the sum
+// of squares 5.44 -> 5.94 TB/s (non-temporal hints made no difference).
+unsigned ew_blocks(size_t n4, size_t per_cu = 128) {
   size_t nb = (n4 + EW_THREADS - 1) / EW_THREADS;
-  const size_t cap = 256 * 8;  // 8 blocks per CU on 256 CUs
+  const size_t cap = 256 * per_cu;
   if (nb > cap) nb = cap;
   if (nb < 1) nb = 1;
   return (unsigned)nb;
 }
+
+// The gradient norm keeps 8 blocks per CU: its block partials are summed by
+// one block afterwards, and 32768 of them cost more than the wider grid saves.
+unsigned norm_blocks(size_t n4) { return ew_blocks(n4, 8); }
 
 __global__ void __launch_bounds__(EW_THREADS) gelu_fwd_kernel(const floatx4* __restrict__ x,
                                                               floatx4* __restrict__ y, size_t n4) {
@@ -302,7 +310,7 @@ extern "C" bt_status bt_adamw_step(float* p, const float* g, float* m, float* v,
 }
 
 extern "C" size_t bt_grad_norm_ws_bytes(size_t n) {
-  return align_up((size_t)ew_blocks(n / 4) * sizeof(double), 256);
+  return align_up((size_t)norm_blocks(n / 4) * sizeof(double), 256);
 }
 
 extern "C" bt_status bt_grad_norm_clip(const float* g, size_t n, float clip, float* out_norm, float* out_coef,
@@ -315,7 +323,7 @@ extern "C" bt_status bt_grad_norm_clip(const float* g, size_t n, float clip, flo
   BT_RETURN_IF(!ws || ws_bytes < need, BT_EWORKSPACE, "bt_grad_norm_clip: workspace of %zu bytes needed (got %zu)",
                need, ws_bytes);
   const size_t n4 = n / 4;
-  const unsigned nb = ew_blocks(n4);
+  const unsigned nb = norm_blocks(n4);
   hipStream_t s = as_stream(stream);
   double* part = static_cast<double*>(ws);
   hipLaunchKernelGGL(sumsq_kernel, dim3(nb), dim3(EW_THREADS), 0, s, reinterpret_cast<const floatx4*>(g), n4, part);

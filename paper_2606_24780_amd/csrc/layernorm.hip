@@ -69,27 +69,30 @@ __global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ x
   }
 }
 
-// Backward block: W waves (16 for rows up to 512 floats, fewer for wider
+// Backward block: W waves (16 for rows up to 256 floats, fewer for wider
 // rows so the registers suffice); each wave takes rows r0+w, r0+w+W, ... of
 // the block's contiguous chunk, two rows at a time when they fit (both
 // rows' loads issued before either row's reductions).
 template <int NV>
 struct BwdWaves {
-  static constexpr int value = NV <= 2 ? 16 : (NV <= 4 ? 8 : 4);
+  static constexpr int value = NV <= 1 ? 16 : (NV <= 4 ? 8 : 4);
 };
 
 template <int NV>
 struct LnRow {
   floatx4 d[NV], xh[NV];  // dy and xhat of the row (g = dy * gamma is recomputed)
+  floatx4 old[NV];        // dx before this call (accumulating calls), loaded with dy and x
   float mg, mgx, rs;
 };
 
 template <int NV>
 __device__ __forceinline__ void ln_row_load(LnRow<NV>& r, const float* dy, const float* __restrict__ x,
                                             const float* __restrict__ mean, const float* __restrict__ rstd,
-                                            const floatx4 (&gam)[NV], int row, int C4, int lane) {
+                                            const float* dx, bool accumulate, const floatx4 (&gam)[NV],
+                                            int row, int C4, int lane) {
   const floatx4* dyr = reinterpret_cast<const floatx4*>(dy + (long long)row * 4 * C4);
   const floatx4* xr = reinterpret_cast<const floatx4*>(x + (long long)row * 4 * C4);
+  const floatx4* dxr = reinterpret_cast<const floatx4*>(dx + (long long)row * 4 * C4);
   const float mu = mean[row];
   r.rs = rstd[row];
   floatx4 xv[NV];
@@ -98,6 +101,7 @@ __device__ __forceinline__ void ln_row_load(LnRow<NV>& r, const float* dy, const
     const int c = lane + 64 * i;
     r.d[i] = c < C4 ? dyr[c] : floatx4{0.f, 0.f, 0.f, 0.f};
     xv[i] = c < C4 ? xr[c] : floatx4{0.f, 0.f, 0.f, 0.f};
+    r.old[i] = (accumulate && c < C4) ? dxr[c] : floatx4{0.f, 0.f, 0.f, 0.f};
   }
   float s1 = 0.f, s2 = 0.f;
 #pragma unroll
@@ -128,7 +132,7 @@ __device__ __forceinline__ void ln_row_store(const LnRow<NV>& r, const floatx4 (
       floatx4 o;
 #pragma unroll
       for (int k = 0; k < 4; ++k) o[k] = r.rs * (r.d[i][k] * gam[i][k] - mg - r.xh[i][k] * mgx);
-      if (dx_beta != 0.f) o += dxr[c];
+      if (dx_beta != 0.f) o += r.old[i];
       dxr[c] = o;
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
@@ -163,12 +167,13 @@ __global__ void __launch_bounds__(64 * BWD_WAVES) ln_bwd_kernel(const float* dy,
   }
   const int r0 = blockIdx.x * rows_per_block;
   const int r1 = min(M, r0 + rows_per_block);
+  const bool acc = dx_beta != 0.f;
   int row = r0 + wave;
   if (NV <= 4) {
     for (; row + BWD_WAVES < r1; row += 2 * BWD_WAVES) {
       LnRow<NV> a, b;
-      ln_row_load<NV>(a, dy, x, mean, rstd, gam, row, C4, lane);
-      ln_row_load<NV>(b, dy, x, mean, rstd, gam, row + BWD_WAVES, C4, lane);
+      ln_row_load<NV>(a, dy, x, mean, rstd, dx, acc, gam, row, C4, lane);
+      ln_row_load<NV>(b, dy, x, mean, rstd, dx, acc, gam, row + BWD_WAVES, C4, lane);
       a.mg = wave_sum(a.mg);
       b.mg = wave_sum(b.mg);
       a.mgx = wave_sum(a.mgx);
@@ -179,7 +184,7 @@ __global__ void __launch_bounds__(64 * BWD_WAVES) ln_bwd_kernel(const float* dy,
   }
   for (; row < r1; row += BWD_WAVES) {
     LnRow<NV> a;
-    ln_row_load<NV>(a, dy, x, mean, rstd, gam, row, C4, lane);
+    ln_row_load<NV>(a, dy, x, mean, rstd, dx, acc, gam, row, C4, lane);
     a.mg = wave_sum(a.mg);
     a.mgx = wave_sum(a.mgx);
     ln_row_store<NV>(a, gam, dx, row, C4, lane, invC, dx_beta, acc_dg, acc_db);
@@ -213,7 +218,7 @@ int ln_nv(int C) { return (C / 4 + 63) / 64; }
 // Waves per backward block for a row width (BwdWaves of the dispatched NV).
 int ln_bwd_waves(int C) {
   const int nv = ln_nv(C);
-  return nv <= 2 ? 16 : (nv <= 4 ? 8 : 4);
+  return nv <= 1 ? 16 : (nv <= 4 ? 8 : 4);
 }
 
 // Backward blocks: about two rows per wave (a block of W waves takes >= 2W

@@ -47,7 +47,10 @@ __global__ void __launch_bounds__(XT) xent_row_kernel(float* logits, const int32
 #pragma unroll
   for (int i = 0; i < NPT; ++i) {
     const int c4 = tid + XT * i;
-    z[i] = c4 < V4 ? zr[c4] : floatx4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+    // the fused pass reads and overwrites each logit exactly once: streaming
+    // (non-temporal) accesses keep the 3.3 GB row stream out of the caches
+    z[i] = c4 < V4 ? (MODE == 1 ? __builtin_nontemporal_load(zr + c4) : zr[c4])
+                   : floatx4{-INFINITY, -INFINITY, -INFINITY, -INFINITY};
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       if (4 * c4 + k >= V) z[i][k] = -INFINITY;  // padded columns are outside the softmax
@@ -86,7 +89,7 @@ __global__ void __launch_bounds__(XT) xent_row_kernel(float* logits, const int32
           const int c = 4 * c4 + k;
           o[k] = c < V ? z[i][k] * inv - (c == y ? scale : 0.f) : 0.f;
         }
-        dr[c4] = o;
+        __builtin_nontemporal_store(o, dr + c4);
       }
     }
   }
