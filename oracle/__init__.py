@@ -15,4 +15,4 @@ invariants, brute force or an independent library routine (see the
 ``tests/test_oracle_*.py`` suites); the full 124M step is pinned only through
 its parts plus the zero-embedding ln(V) loss.
 """
-from . import ops, gpt2  # noqa: F401
+from . import ops, gpt2, context_parallel  # noqa: F401
