@@ -133,6 +133,99 @@ size_t bt_attention_bwd_ws_bytes(int B, int T, int H, int hd);
 size_t bt_attention_bwd_ws_min_bytes(int B, int T, int H, int hd);
 
 /*
+ * ---- Context parallelism: one rank's share of ring attention ----
+ * Section "Context Parallelism": the sequence is spread over W ranks; the
+ * key/value shards travel around a ring; at each step a rank attends its
+ * local queries to the shard it holds, giving a partial output and its
+ * log-sum-exp, and folds them into its running (out, lse) with the
+ * sigmoid-scaled update; the backward recomputes the scores shard by shard
+ * and sends each shard's dK/dV around the ring with it.  Token chunks are
+ * rearranged once where the data is loaded so that every rank carries the
+ * same causal work: the sequence is cut into 2W equal chunks and rank r
+ * holds chunks r and 2W-1-r.  These calls are the per-rank kernels; moving
+ * the shards between GPUs is the caller's.
+ *
+ * Positions: a side's rows are n (1 or 2) contiguous segments of `seg`
+ * tokens; segment i starts at global token position pos[i].  Key j is visible
+ * to query i iff position(j) <= position(i).
+ */
+typedef struct {
+  int seg;       /* tokens per segment: a positive multiple of 128 */
+  int n_q, n_k;  /* segments of the query rows and of the key/value rows: 1 or 2 */
+  int q_pos[2];  /* global position of each query segment's first token (multiple of 32, >= 0) */
+  int k_pos[2];  /* same for the key/value segments */
+} bt_cp_segments;
+
+/*
+ * Segments of rank `rank`'s queries and of the shard owned by rank `shard`
+ * under the load-balanced split above (seg = T / (2W), two segments a side).
+ * Host only; writes *out.  T must be a multiple of 2 W 128 (BT_ESHAPE);
+ * ranks outside [0, W): BT_EINVAL.
+ */
+bt_status bt_cp_rank_segments(int T, int W, int rank, int shard, bt_cp_segments* out);
+
+/*
+ * The rearrangement at the data-loading boundary: local [B, T/W] (int32,
+ * device, written) = rank `rank`'s two chunks of each row of tokens [B, T]
+ * (int32, device), in order.  Same size rules as bt_cp_rank_segments.
+ */
+bt_status bt_cp_shard_tokens(const int32_t* tokens, int32_t* local, int B, int T, int W, int rank,
+                             void* stream);
+
+/*
+ * Forward of one ring step.  Queries: the Q part of the rank's local qkv
+ * [B, Tq, 3, H, hd] with Tq = n_q seg.  Keys and values of the shard: row t of
+ * batch b at kv + (b Tk + t) kv_stride (K) and + H hd (V), Tk = n_k seg; a
+ * view into the owner's qkv (kv = qkv + H hd, kv_stride = 3 H hd) or a packed
+ * [B, Tk, 2, H, hd] buffer (kv_stride = 2 H hd) both fit.  kv_stride a
+ * multiple of 4 and >= 2 H hd.
+ *   merge = 0: out [B, Tq, H, hd] and lse [B, H, Tq] are written with this
+ *              shard's attention; a query with no visible key gets a zero
+ *              row and lse = -inf.
+ *   merge = 1: (out, lse) hold the running state and are updated in place:
+ *              out <- out - sigmoid(blse - lse) (out - bout),
+ *              lse <- lse - log sigmoid(lse - blse); a row whose block is
+ *              empty keeps its state, a row whose state is empty (lse = -inf)
+ *              takes the block.
+ * hd as bt_attention_fwd.  Errors: BT_ESHAPE (segments, sizes), BT_EALIGN
+ * (qkv, out, kv not 16-byte aligned), BT_EINVAL (NULL, merge not 0/1).
+ */
+bt_status bt_attention_block_fwd(const float* qkv, const float* kv, long long kv_stride, float* out,
+                                 float* lse, int merge, int B, int H, int hd,
+                                 const bt_cp_segments* segs, void* stream);
+
+/*
+ * The sigmoid-scaled update on its own, for a partial result computed
+ * elsewhere: out [B, T, H, hd], lse [B, H, T] updated in place by block_out,
+ * block_lse of the same layout (rules as merge = 1 above).
+ */
+bt_status bt_attention_lse_merge(float* out, float* lse, const float* block_out, const float* block_lse,
+                                 int B, int T, int H, int hd, void* stream);
+
+/*
+ * D = rowsum(dout o out) per head, D [B, H, T] (written), from the rank's
+ * final output out and its gradient dout [B, T, H, hd].  Computed once per
+ * rank before the backward ring.
+ */
+bt_status bt_attention_rowdot(const float* dout, const float* out, float* D, int B, int T, int H, int hd,
+                              void* stream);
+
+/*
+ * Backward of one ring step, given the final lse [B, H, Tq] (after every
+ * merge) and D: P = exp(S - lse) on visible entries, dV = P^T dO,
+ * dS = P o (dO V^T - D), dQ = dS K / sqrt(hd), dK = dS^T Q / sqrt(hd).
+ * dQ goes to the Q part of dqkv [B, Tq, 3, H, hd] (its K and V parts are not
+ * touched); dK and dV of the shard go to dkv, laid out as kv (same
+ * kv_stride).  accumulate: bit 0 adds into dQ, bit 1 adds into dK/dV (else
+ * they are overwritten).  Deterministic; no workspace.  Errors as
+ * bt_attention_block_fwd; gradients must not alias inputs (BT_EINVAL).
+ */
+bt_status bt_attention_block_bwd(const float* dout, const float* qkv, const float* kv, long long kv_stride,
+                                 const float* lse, const float* D, float* dqkv, float* dkv,
+                                 int accumulate, int B, int H, int hd, const bt_cp_segments* segs,
+                                 void* stream);
+
+/*
  * LayerNorm forward over the last dimension (pre-normalised blocks of the
  * GPT-2 architecture figure; appendix "LayerNorm Forward"):
  *   mean = sum_c x / C, var = sum_c (x - mean)^2 / C, rstd = 1/sqrt(var + eps)

@@ -56,6 +56,25 @@ class GPT2ConfigC(_c.Structure):
                 ("weight_decay", f64), ("grad_clip", f64)]
 
 
+class CPSegments(_c.Structure):
+    """bt_cp_segments: a rank's query rows and a shard's key/value rows as 1 or
+    2 segments of `seg` tokens starting at global positions q_pos / k_pos."""
+    _fields_ = [("seg", i32), ("n_q", i32), ("n_k", i32), ("q_pos", i32 * 2), ("k_pos", i32 * 2)]
+
+
+def cp_segments(seg, q_pos, k_pos) -> CPSegments:
+    """Build a CPSegments from position lists (1 or 2 entries per side)."""
+    g = CPSegments()
+    g.seg, g.n_q, g.n_k = seg, len(q_pos), len(k_pos)
+    for i, v in enumerate(q_pos):
+        g.q_pos[i] = v
+    for i, v in enumerate(k_pos):
+        g.k_pos[i] = v
+    return g
+
+
+i64 = _c.c_longlong
+
 _SIGS = {
     "bt_status_str": (_c.c_char_p, [i32]),
     "bt_last_error": (_c.c_char_p, []),
@@ -66,6 +85,13 @@ _SIGS = {
     "bt_attention_bwd": (i32, [vp, vp, vp, vp, vp, vp, sz, i32, i32, i32, i32, vp]),
     "bt_attention_bwd_ws_bytes": (sz, [i32, i32, i32, i32]),
     "bt_attention_bwd_ws_min_bytes": (sz, [i32, i32, i32, i32]),
+    "bt_cp_rank_segments": (i32, [i32, i32, i32, i32, _c.POINTER(CPSegments)]),
+    "bt_cp_shard_tokens": (i32, [vp, vp, i32, i32, i32, i32, vp]),
+    "bt_attention_block_fwd": (i32, [vp, vp, i64, vp, vp, i32, i32, i32, i32, _c.POINTER(CPSegments), vp]),
+    "bt_attention_lse_merge": (i32, [vp, vp, vp, vp, i32, i32, i32, i32, vp]),
+    "bt_attention_rowdot": (i32, [vp, vp, vp, i32, i32, i32, i32, vp]),
+    "bt_attention_block_bwd": (i32, [vp, vp, vp, i64, vp, vp, vp, vp, i32, i32, i32, i32,
+                                     _c.POINTER(CPSegments), vp]),
     "bt_layernorm_fwd": (i32, [vp, vp, vp, vp, vp, vp, i32, i32, f32, vp]),
     "bt_layernorm_bwd": (i32, [vp, vp, vp, vp, vp, vp, vp, vp, f32, f32, vp, sz, i32, i32, vp]),
     "bt_layernorm_bwd_ws_bytes": (sz, [i32, i32]),
@@ -191,6 +217,39 @@ def bt_attention_bwd(dout, qkv, out, lse, dqkv, B, T, H, hd, ws=None, stream=Non
     _check(L.bt_attention_bwd(_p(dout), _p(qkv), _p(out), _p(lse), _p(dqkv), _p(w),
                               0 if w is None else w.numel() * w.element_size(), B, T, H, hd,
                               _stream(stream)), "bt_attention_bwd")
+
+
+def bt_cp_rank_segments(T, W, rank, shard) -> CPSegments:
+    g = CPSegments()
+    _check(lib().bt_cp_rank_segments(T, W, rank, shard, _c.byref(g)), "bt_cp_rank_segments")
+    return g
+
+
+def bt_cp_shard_tokens(tokens, local, B, T, W, rank, stream=None):
+    _check(lib().bt_cp_shard_tokens(_p(tokens), _p(local), B, T, W, rank, _stream(stream)),
+           "bt_cp_shard_tokens")
+
+
+def bt_attention_block_fwd(qkv, kv, kv_stride, out, lse, merge, B, H, hd, segs, stream=None):
+    _check(lib().bt_attention_block_fwd(_p(qkv), _p(kv), kv_stride, _p(out), _p(lse), int(merge), B, H, hd,
+                                        _c.byref(segs), _stream(stream)), "bt_attention_block_fwd")
+
+
+def bt_attention_lse_merge(out, lse, block_out, block_lse, B, T, H, hd, stream=None):
+    _check(lib().bt_attention_lse_merge(_p(out), _p(lse), _p(block_out), _p(block_lse), B, T, H, hd,
+                                        _stream(stream)), "bt_attention_lse_merge")
+
+
+def bt_attention_rowdot(dout, out, D, B, T, H, hd, stream=None):
+    _check(lib().bt_attention_rowdot(_p(dout), _p(out), _p(D), B, T, H, hd, _stream(stream)),
+           "bt_attention_rowdot")
+
+
+def bt_attention_block_bwd(dout, qkv, kv, kv_stride, lse, D, dqkv, dkv, accumulate, B, H, hd, segs,
+                           stream=None):
+    _check(lib().bt_attention_block_bwd(_p(dout), _p(qkv), _p(kv), kv_stride, _p(lse), _p(D), _p(dqkv),
+                                        _p(dkv), int(accumulate), B, H, hd, _c.byref(segs),
+                                        _stream(stream)), "bt_attention_block_bwd")
 
 
 def bt_layernorm_fwd(x, gamma, beta, y, mean, rstd, M, C, eps=1e-5, stream=None):

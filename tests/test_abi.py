@@ -120,6 +120,59 @@ def test_attention_workspace_sizes(lib):
                                 1, 16, 1, 64, None) == BT_EWORKSPACE
 
 
+def test_cp_rank_segments_match_oracle_positions(lib):
+    """The library's description of a rank's rows under the load-balanced
+    split names the same global positions as the oracle's rearrangement."""
+    from oracle import context_parallel as cp
+    for T, W in [(256, 1), (1024, 2), (2048, 4), (16384, 8)]:
+        for r in range(W):
+            for s_ in (r, (r + 1) % W):
+                g = bt.CPSegments()
+                assert lib.bt_cp_rank_segments(T, W, r, s_, ctypes.byref(g)) == BT_OK
+                assert g.seg == T // (2 * W) and g.n_q == 2 and g.n_k == 2
+
+                def rows(pos):
+                    return np.concatenate([np.arange(p, p + g.seg) for p in pos])
+                assert np.array_equal(rows(g.q_pos), cp.rank_positions(T, W, r))
+                assert np.array_equal(rows(g.k_pos), cp.rank_positions(T, W, s_))
+    g = bt.CPSegments()
+    assert lib.bt_cp_rank_segments(1000, 2, 0, 0, ctypes.byref(g)) == BT_ESHAPE
+    assert lib.bt_cp_rank_segments(1024, 2, 2, 0, ctypes.byref(g)) == BT_EINVAL
+    assert lib.bt_cp_rank_segments(1024, 2, 0, -1, ctypes.byref(g)) == BT_EINVAL
+    assert lib.bt_cp_rank_segments(1024, 2, 0, 0, None) == BT_EINVAL
+    assert lib.bt_cp_shard_tokens(FAKE, FAKE + 4096, 1, 1000, 2, 0, None) == BT_ESHAPE
+
+
+def test_cp_block_validation(lib):
+    def segs(seg=128, q=(0, 384), k=(128, 256)):
+        return ctypes.byref(bt.cp_segments(seg, list(q), list(k)))
+    H, hd = 2, 64
+    fwd = lambda g, kvs=2 * H * hd, merge=0: lib.bt_attention_block_fwd(
+        FAKE, FAKE + 65536, kvs, FAKE + 131072, FAKE + 196608, merge, 1, H, hd, g, None)
+    assert fwd(segs(seg=100)) == BT_ESHAPE
+    assert fwd(segs(seg=0)) == BT_ESHAPE
+    assert fwd(segs(q=(0, 16))) == BT_ESHAPE             # position not a multiple of 32
+    assert fwd(segs(k=(-128,))) == BT_ESHAPE
+    g3 = bt.cp_segments(128, [0, 128], [0])
+    g3.n_q = 3
+    assert fwd(ctypes.byref(g3)) == BT_ESHAPE
+    assert fwd(segs(), kvs=2 * H * hd - 4) == BT_ESHAPE  # K and V rows overlap
+    assert fwd(segs(), kvs=2 * H * hd + 2) == BT_ESHAPE  # not a multiple of 4
+    assert fwd(segs(), merge=2) == BT_EINVAL
+    assert fwd(None) == BT_EINVAL
+    assert lib.bt_attention_block_fwd(FAKE, FAKE_MIS, 2 * H * hd, FAKE + 131072, FAKE + 196608, 0, 1, H, hd,
+                                      segs(), None) == BT_EALIGN
+    bwd = lambda g, acc=0, dkv=FAKE + 262144: lib.bt_attention_block_bwd(
+        FAKE, FAKE + 65536, FAKE + 131072, 2 * H * hd, FAKE + 196608, FAKE + 200000, FAKE + 327680, dkv, acc,
+        1, H, hd, g, None)
+    assert bwd(segs(), acc=4) == BT_EINVAL
+    assert bwd(segs(), dkv=FAKE + 131072) == BT_EINVAL    # dkv aliases kv
+    assert bwd(segs(seg=64)) == BT_ESHAPE
+    assert lib.bt_attention_lse_merge(FAKE, FAKE, FAKE, FAKE, 1, 16, 2, 6, None) == BT_ESHAPE
+    assert lib.bt_attention_lse_merge(FAKE, FAKE, None, FAKE, 1, 16, 2, 8, None) == BT_EINVAL
+    assert lib.bt_attention_rowdot(FAKE, FAKE, FAKE, 1, 16, 2, 132, None) == BT_ESHAPE
+
+
 def test_gpt2_context_validation(lib):
     cfg = bt.make_config(synth.TINY, synth.HP_TINY)
     need = lib.bt_gpt2_workspace_bytes(ctypes.byref(cfg), 2, 32)

@@ -1,0 +1,266 @@
+"""Context-parallel ring attention, one rank's share (section "Context
+Parallelism"), through the C ABI against the float64 oracle.
+
+* one ring step's forward for every kind of shard pair (own shard, earlier
+  and later shards, a shard with fully masked queries), two key/value layouts
+  (a view into the owner's qkv, a packed [B, T, 2, H, hd] buffer), head dims
+  32 / 64 / 96 / 128, and single-segment positions that are multiples of 32
+  but not of 128;
+* the merge fused into the forward and the standalone merge, including rows
+  whose state or block is empty (lse = -inf);
+* the whole ring emulated on one GPU (all ranks, forward and backward) against
+  the oracle's ring, which equals plain causal attention;
+* the token rearrangement at the data-loading boundary (bit-exact);
+* the GPT-2 124M long-context shape (B = 2, T = 16384, H = 12) over W = 8
+  ranks: the ring against the library's single-GPU causal attention on the
+  whole sequence, and sampled rows against the oracle row by row.
+
+Bars: outputs and lse <= 1e-5 of max-abs, gradients <= 1e-4 of max-abs;
+empty rows exactly (0, -inf)."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import context_parallel as cp
+from oracle import ops
+from paper_2606_24780_amd import bt, ring
+from tests.gpu_util import assert_close_maxabs, dev, host, say, torch_gpu
+
+pytestmark = pytest.mark.gpu
+RNG = np.random.Generator(np.random.PCG64(24780))
+
+
+def _heads(a, H):
+    """[B, T, H, hd] -> [B, H, T, hd] float64."""
+    return np.asarray(a, np.float64).transpose(0, 2, 1, 3)
+
+
+def _local(qkv, pos):
+    return np.ascontiguousarray(qkv[:, pos])
+
+
+def _check_block(out, lse, r_out, r_lse, what):
+    empty = ~np.isfinite(r_lse)
+    assert np.array_equal(~np.isfinite(lse), empty), f"{what}: empty rows differ"
+    assert np.all(lse[empty] == -np.inf)
+    assert np.all(out.transpose(0, 2, 1, 3)[empty] == 0), f"{what}: empty rows not zero"
+    assert_close_maxabs(out, r_out.transpose(0, 2, 1, 3), 1e-5, f"{what} out")
+    if (~empty).any():
+        assert_close_maxabs(lse[~empty], r_lse[~empty], 1e-5, f"{what} lse")
+
+
+@pytest.mark.parametrize("B,T,W,H,hd,pairs", [
+    (2, 1024, 2, 2, 64, [(0, 0), (0, 1), (1, 0), (1, 1)]),
+    (1, 2048, 4, 2, 32, [(0, 3), (3, 0), (1, 2), (2, 2), (3, 1)]),
+    (1, 1024, 2, 2, 128, [(1, 0), (0, 1)]),
+    (1, 1536, 3, 1, 96, [(2, 0), (0, 2), (1, 1)]),
+])
+@pytest.mark.parametrize("packed", [False, True])
+def test_block_fwd_vs_oracle(B, T, W, H, hd, pairs, packed):
+    torch = torch_gpu()
+    C = H * hd
+    qkv = RNG.standard_normal((B, T, 3, H, hd)).astype(np.float32)
+    q, k, v = ops.split_qkv(qkv, H)
+    for r, s in pairs:
+        say(f"block fwd B={B} T={T} W={W} H={H} hd={hd} rank {r} shard {s} packed={packed}")
+        pr, ps = cp.rank_positions(T, W, r), cp.rank_positions(T, W, s)
+        Tl = len(pr)
+        qkv_r = dev(torch, _local(qkv, pr).reshape(B * Tl, 3 * C))
+        if packed:
+            kv = dev(torch, _local(qkv, ps)[:, :, 1:].reshape(B * Tl, 2 * C))
+            kv_ptr, ks = kv, 2 * C
+        else:
+            qkv_s = dev(torch, _local(qkv, ps).reshape(B * Tl, 3 * C))
+            kv_ptr, ks = qkv_s[:, C:], 3 * C
+        out = torch.full((B * Tl, C), float("nan"), device="cuda")
+        lse = torch.full((B, H, Tl), float("nan"), device="cuda")
+        segs = bt.bt_cp_rank_segments(T, W, r, s)
+        bt.bt_attention_block_fwd(qkv_r, kv_ptr, ks, out, lse, 0, B, H, hd, segs)
+        r_out, r_lse = cp.block_attention_fwd(q[:, :, pr], k[:, :, ps], v[:, :, ps], pr, ps)
+        _check_block(host(out).reshape(B, Tl, H, hd), host(lse), r_out, r_lse, f"r{r} s{s}")
+
+
+def test_block_fwd_single_segments_unaligned_to_tiles():
+    """One segment a side; positions multiples of 32 but not of 128, so key
+    tiles straddle the queries' 128-row tiles."""
+    torch = torch_gpu()
+    B, H, hd, seg = 1, 2, 64, 256
+    C = H * hd
+    for qp, kp in [(512, 160), (160, 512), (96, 96), (0, 224)]:
+        say(f"single segments q_pos={qp} k_pos={kp}")
+        qkv_q = RNG.standard_normal((B, seg, 3, H, hd)).astype(np.float32)
+        qkv_k = RNG.standard_normal((B, seg, 3, H, hd)).astype(np.float32)
+        dq, dk = dev(torch, qkv_q.reshape(B * seg, 3 * C)), dev(torch, qkv_k.reshape(B * seg, 3 * C))
+        out = torch.empty((B * seg, C), device="cuda")
+        lse = torch.empty((B, H, seg), device="cuda")
+        segs = bt.cp_segments(seg, [qp], [kp])
+        bt.bt_attention_block_fwd(dq, dk[:, C:], 3 * C, out, lse, 0, B, H, hd, segs)
+        pq, pk = qp + np.arange(seg), kp + np.arange(seg)
+        q = ops.split_qkv(qkv_q, H)[0]
+        _, k, v = ops.split_qkv(qkv_k, H)
+        r_out, r_lse = cp.block_attention_fwd(q, k, v, pq, pk)
+        _check_block(host(out).reshape(B, seg, H, hd), host(lse), r_out, r_lse, f"q{qp} k{kp}")
+
+
+def test_fused_merge_vs_oracle():
+    """merge = 1 folds the shard into a running state, including rows whose
+    state is empty (they take the block) and rows whose block is empty (they
+    keep the state)."""
+    torch = torch_gpu()
+    B, T, W, H, hd = 2, 2048, 4, 2, 64
+    C = H * hd
+    qkv = RNG.standard_normal((B, T, 3, H, hd)).astype(np.float32)
+    q, k, v = ops.split_qkv(qkv, H)
+    r, s = 1, 3  # shard 3: chunks 3 and 4 -> rank 1's first chunk sees nothing of it
+    pr, ps = cp.rank_positions(T, W, r), cp.rank_positions(T, W, s)
+    Tl = len(pr)
+    st_out = RNG.standard_normal((B, H, Tl, hd))
+    st_lse = RNG.standard_normal((B, H, Tl)) * 3 + 5
+    st_lse[:, :, 300:400] = -np.inf  # empty state rows (second chunk: they see shard 3)
+    st_out[:, :, 300:400] = 0
+    st_out, st_lse = st_out.astype(np.float32).astype(np.float64), st_lse.astype(np.float32).astype(np.float64)
+    out = dev(torch, st_out.transpose(0, 2, 1, 3).reshape(B * Tl, C))
+    lse = dev(torch, st_lse)
+    qkv_r = dev(torch, _local(qkv, pr).reshape(B * Tl, 3 * C))
+    qkv_s = dev(torch, _local(qkv, ps).reshape(B * Tl, 3 * C))
+    say("fused merge")
+    bt.bt_attention_block_fwd(qkv_r, qkv_s[:, C:], 3 * C, out, lse, 1, B, H, hd, bt.bt_cp_rank_segments(T, W, r, s))
+    b_out, b_lse = cp.block_attention_fwd(q[:, :, pr], k[:, :, ps], v[:, :, ps], pr, ps)
+    assert (~np.isfinite(b_lse)).any() and np.isfinite(b_lse).any()
+    m_out, m_lse = cp.lse_merge(st_out, st_lse, b_out, b_lse)
+    g_out, g_lse = host(out).reshape(B, Tl, H, hd), host(lse)
+    keep = ~np.isfinite(b_lse)
+    assert np.array_equal(g_lse[keep], st_lse[keep])  # untouched rows: bitwise
+    assert np.array_equal(g_out.transpose(0, 2, 1, 3)[keep], st_out[keep])
+    assert_close_maxabs(g_out, m_out.transpose(0, 2, 1, 3), 1e-5, "merged out")
+    assert_close_maxabs(g_lse, m_lse, 1e-5, "merged lse")
+
+
+def test_lse_merge_standalone_vs_oracle():
+    torch = torch_gpu()
+    B, T, H, hd = 2, 200, 3, 40
+    o = RNG.standard_normal((B, T, H, hd)).astype(np.float32)
+    bo = RNG.standard_normal((B, T, H, hd)).astype(np.float32)
+    l = (RNG.standard_normal((B, H, T)) * 4).astype(np.float32)
+    bl = (RNG.standard_normal((B, H, T)) * 4).astype(np.float32)
+    l[0, 1, 5:9] = -np.inf
+    bl[1, 2, 50:60] = -np.inf
+    l[1, 0, 70] = bl[1, 0, 70] = -np.inf
+    bl[0, 0, 100:110] = l[0, 0, 100:110] + 60   # large gaps both ways
+    bl[0, 0, 110:120] = l[0, 0, 110:120] - 60
+    o[1, 70, 0] = bo[1, 70, 0] = 0   # row (b 1, h 0, t 70): state and block both empty
+    go, gl = dev(torch, o), dev(torch, l)
+    say("standalone merge")
+    bt.bt_attention_lse_merge(go, gl, dev(torch, bo), dev(torch, bl), B, T, H, hd)
+    r_o, r_l = cp.lse_merge(_heads(o, H), l, _heads(bo, H), bl)
+    g_o, g_l = host(go), host(gl)
+    assert np.array_equal(np.isfinite(g_l), np.isfinite(r_l))
+    assert g_l[1, 0, 70] == -np.inf and np.all(g_o[1, 70, 0] == 0)
+    fin = np.isfinite(r_l)
+    assert_close_maxabs(g_l[fin], r_l[fin], 1e-6, "lse")
+    assert_close_maxabs(g_o, r_o.transpose(0, 2, 1, 3), 1e-5, "out")
+
+
+def _gpu_ring(torch, qkv, dout, T, W, H, hd, packed_grad=False):
+    """All ranks on one GPU through the ring schedule; returns global-order
+    (out, lse, dqkv)."""
+    B = qkv.shape[0]
+    C = H * hd
+    pos = [cp.rank_positions(T, W, r) for r in range(W)]
+    Tl = T // W
+    qkv_l = [dev(torch, _local(qkv, p).reshape(B * Tl, 3 * C)) for p in pos]
+    out = [torch.empty((B * Tl, C), device="cuda") for _ in range(W)]
+    lse = [torch.empty((B, H, Tl), device="cuda") for _ in range(W)]
+    do_l = [dev(torch, _local(dout, p).reshape(B * Tl, C)) for p in pos] if dout is not None else None
+    D = [torch.empty((B, H, Tl), device="cuda") for _ in range(W)]
+    dq = [torch.full((B * Tl, 3 * C), float("nan"), device="cuda") for _ in range(W)]
+    ring.emulate(W, T, B, H, hd, qkv_l, out, lse, lambda s: (qkv_l[s][:, C:], 3 * C),
+                 dout=do_l, D=D, dqkv=dq, dkv_of=lambda s: dq[s][:, C:])
+    g_out = np.empty((B, T, H, hd))
+    g_lse = np.empty((B, H, T))
+    g_d = np.empty((B, T, 3, H, hd))
+    for r, p in enumerate(pos):
+        g_out[:, p] = host(out[r]).reshape(B, Tl, H, hd)
+        g_lse[:, :, p] = host(lse[r])
+        if dout is not None:
+            g_d[:, p] = host(dq[r]).reshape(B, Tl, 3, H, hd)
+    return g_out, g_lse, g_d
+
+
+@pytest.mark.parametrize("B,T,W,H,hd", [(1, 1024, 2, 2, 64), (2, 2048, 4, 2, 64), (1, 768, 3, 2, 128)])
+def test_ring_emulation_vs_oracle(B, T, W, H, hd):
+    torch = torch_gpu()
+    qkv = RNG.standard_normal((B, T, 3, H, hd)).astype(np.float32)
+    dout = RNG.standard_normal((B, T, H, hd)).astype(np.float32)
+    say(f"ring emulation B={B} T={T} W={W} H={H} hd={hd}")
+    g_out, g_lse, g_d = _gpu_ring(torch, qkv, dout, T, W, H, hd)
+    say("oracle ring")
+    r_out, r_lse = cp.ring_attention_fwd(qkv, H, W)
+    r_d = cp.ring_attention_bwd(dout, qkv, H, W)
+    assert_close_maxabs(g_out, r_out, 1e-5, "ring out")
+    assert_close_maxabs(g_lse, r_lse, 1e-5, "ring lse")
+    for i, n in enumerate("QKV"):
+        assert_close_maxabs(g_d[:, :, i], r_d[:, :, i], 1e-4, f"ring d{n}", scale=np.abs(r_d).max())
+
+
+def test_shard_tokens_bitwise():
+    torch = torch_gpu()
+    B, T = 3, 4096
+    tok = RNG.integers(0, 50257, size=(B, T)).astype(np.int32)
+    d = dev(torch, tok)
+    for W in (1, 2, 8):
+        for r in range(W):
+            loc = torch.full((B, T // W), -1, dtype=torch.int32, device="cuda")
+            bt.bt_cp_shard_tokens(d, loc, B, T, W, r)
+            torch.cuda.synchronize()
+            assert np.array_equal(loc.cpu().numpy(), cp.shard_tokens(tok, W, r))
+
+
+@pytest.mark.timeout(900)
+def test_ring_gpt2_124m_longctx_matches_full_attention():
+    """B = 2, T = 16384, H = 12, hd = 64 over W = 8 ranks (2048 local tokens,
+    chunks of 1024)."""
+    torch = torch_gpu()
+    B, T, W, H, hd = 2, 16384, 8, 12, 64
+    C = H * hd
+    qkv = RNG.standard_normal((B, T, 3, H, hd)).astype(np.float32)
+    dout = RNG.standard_normal((B, T, H, hd)).astype(np.float32)
+    say("ring at B=2 T=16384 W=8")
+    g_out, g_lse, g_d = _gpu_ring(torch, qkv, dout, T, W, H, hd)
+    say("single-GPU causal attention on the whole sequence")
+    dq = dev(torch, qkv.reshape(B * T, 3 * C))
+    f_out = torch.empty((B * T, C), device="cuda")
+    f_lse = torch.empty((B, H, T), device="cuda")
+    bt.bt_attention_fwd(dq, f_out, f_lse, B, T, H, hd)
+    f_d = torch.empty_like(dq)
+    bt.bt_attention_bwd(dev(torch, dout.reshape(B * T, C)), dq, f_out, f_lse, f_d, B, T, H, hd, small_ws=True)
+    assert_close_maxabs(g_out, host(f_out).reshape(B, T, H, hd), 1e-5, "ring vs full out")
+    assert_close_maxabs(g_lse, host(f_lse), 1e-5, "ring vs full lse")
+    fd = host(f_d).reshape(B, T, 3, H, hd)
+    for i, n in enumerate("QKV"):
+        assert_close_maxabs(g_d[:, :, i], fd[:, :, i], 1e-4, f"ring vs full d{n}", scale=np.abs(fd).max())
+    say("oracle rows")
+    sq = 1.0 / math.sqrt(hd)
+    dq_rows = []
+    for b, h, t in [(0, 0, 0), (1, 5, 1023), (0, 11, 1024), (1, 3, 8191), (0, 7, 12000), (1, 11, 16383)]:
+        qv = qkv[b, t, 0, h].astype(np.float64)
+        kk = qkv[b, :t + 1, 1, h].astype(np.float64)
+        vv = qkv[b, :t + 1, 2, h].astype(np.float64)
+        s = kk @ qv * sq
+        m = s.max()
+        e = np.exp(s - m)
+        lse_ref = m + math.log(e.sum())
+        o_ref = (e / e.sum()) @ vv
+        assert abs(g_lse[b, h, t] - lse_ref) <= 1e-5 * abs(lse_ref) + 1e-6
+        assert np.abs(g_out[b, t, h] - o_ref).max() <= 1e-5 * max(1.0, np.abs(o_ref).max())
+        # dQ of the row from its own definition: dS_j = P_j (dP_j - D), D = dO . O
+        do = dout[b, t, h].astype(np.float64)
+        p = e / e.sum()
+        ds = p * (vv @ do - do @ o_ref)
+        dq_rows.append((g_d[b, t, 0, h], ds @ kk * sq))
+    # the gradient bar is relative to the tensor's magnitude (the row at t = 0
+    # is exactly zero: one visible key, dS = 0); here the sampled rows' largest
+    scale = max(np.abs(r).max() for _, r in dq_rows)
+    for g, r in dq_rows:
+        assert np.abs(g - r).max() <= 1e-4 * scale
