@@ -43,6 +43,9 @@ def parse():
                     help="2.42b: the largest-trainable-model configuration (B = 2 by default)")
     ap.add_argument("--batch", type=int, default=None, help="default 16 (124M, T <= 1024), else 2")
     ap.add_argument("--seq", type=int, default=1024)
+    ap.add_argument("--cp", type=int, default=0, metavar="W",
+                    help="time one rank's share of context-parallel ring attention over W ranks "
+                         "(GPT-2 124M attention at B=2, T=16384) instead of the training step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=2048)
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -140,6 +143,111 @@ def cpu_baseline(sample_tokens: int):
             "seconds": dt, "host_cpus": os.cpu_count()}
 
 
+def bench_cp(a):
+    """One rank's share of context-parallel ring attention (section "Context
+    Parallelism"): the attention of one GPT-2 124M layer (H = 12, hd = 64) at
+    the long-context shape B = 2, T = 16384, spread over W ranks with the
+    load-balanced two-chunk split.  A step is one rank's forward ring (W
+    block forwards, merged) plus its backward ring (row sums, W block
+    backwards); every rank is timed, all ranks' tensors resident on the one
+    GPU.  The shard exchange between GPUs is not part of this timing."""
+    import numpy as np
+    import torch
+
+    from paper_2606_24780_amd import bt, ring
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    W, B, H, hd = a.cp, (a.batch or 2), 12, 64
+    T = a.seq if a.seq != 1024 else 16384
+    C = H * hd
+    Tl = T // W
+    bt.bt_cp_rank_segments(T, W, 0, 0)  # validates T against W
+    g = torch.Generator(device="cuda").manual_seed(24780)
+    qkv = [torch.randn((B * Tl, 3 * C), generator=g, device="cuda") for _ in range(W)]
+    dout = [torch.randn((B * Tl, C), generator=g, device="cuda") for _ in range(W)]
+    out = [torch.empty((B * Tl, C), device="cuda") for _ in range(W)]
+    lse = [torch.empty((B, H, Tl), device="cuda") for _ in range(W)]
+    D = [torch.empty((B, H, Tl), device="cuda") for _ in range(W)]
+    dq = [torch.empty((B * Tl, 3 * C), device="cuda") for _ in range(W)]
+    kv_of = lambda s: (qkv[s][:, C:], 3 * C)
+    dkv_of = lambda s: dq[s][:, C:]
+    ring.emulate(W, T, B, H, hd, qkv, out, lse, kv_of, dout=dout, D=D, dqkv=dq, dkv_of=dkv_of)
+    torch.cuda.synchronize()
+
+    def fwd(r):
+        for i in range(W):
+            kv, ks = kv_of(ring.shard_at(r, i, W))
+            ring.forward_step(r, i, W, T, B, H, hd, qkv[r], kv, ks, out[r], lse[r])
+
+    def bwd(r):
+        bt.bt_attention_rowdot(dout[r], out[r], D[r], B, Tl, H, hd)
+        for i in range(W):
+            s_ = ring.shard_at(r, i, W)
+            kv, ks = kv_of(s_)
+            ring.backward_step(r, i, W, T, B, H, hd, dout[r], qkv[r], kv, ks, lse[r], D[r], dq[r], dkv_of(s_))
+
+    def timed(fn, reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    for r in range(W):
+        for _ in range(a.warmup):
+            fwd(r)
+            bwd(r)
+    torch.cuda.synchronize()
+    fwd_ms = [timed(lambda: fwd(r), a.steps) for r in range(W)]
+    bwd_ms = [timed(lambda: bwd(r), a.steps) for r in range(W)]
+    rank_ms = [f + b for f, b in zip(fwd_ms, bwd_ms)]
+    # credited work: 4 hd FLOP per visible (query, key) pair forward, 8 hd
+    # backward; the split gives every rank 1/W of the T (T + 1) / 2 pairs
+    pairs = B * H * T * (T + 1) / 2 / W
+    flops = 12 * hd * pairs
+    tflops = [flops / (m / 1e3) / 1e12 for m in rank_ms]
+
+    # the same layer's attention on one GPU over the whole sequence, / W
+    full = torch.randn((B * T, 3 * C), generator=g, device="cuda")
+    f_out = torch.empty((B * T, C), device="cuda")
+    f_lse = torch.empty((B, H, T), device="cuda")
+    f_do = torch.randn((B * T, C), generator=g, device="cuda")
+    f_d = torch.empty_like(full)
+    ws = torch.empty(bt.lib().bt_attention_bwd_ws_bytes(B, T, H, hd), dtype=torch.uint8, device="cuda")
+
+    def whole():
+        bt.bt_attention_fwd(full, f_out, f_lse, B, T, H, hd)
+        bt.bt_attention_bwd(f_do, full, f_out, f_lse, f_d, B, T, H, hd, ws=ws)
+    whole()
+    whole_ms = timed(whole, max(1, a.steps // 2))
+    del ws
+    mean_ms = float(np.mean(rank_ms))
+    tf = flops / (max(rank_ms) / 1e3) / 1e12
+    rec = {
+        "metric": "context-parallel ring attention, one rank's share: forward + backward TFLOP/s on 1 GPU",
+        "value": round(tf, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": round(max(rank_ms), 3), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"one rank of W={W} context-parallel ring attention: GPT-2 124M attention layer "
+                               f"(H={H}, hd={hd}), B={B}, T={T}, {Tl} local tokens in chunks of {Tl // 2}",
+                   "W": W, "batch": B, "seq_len": T, "heads": H, "head_dim": hd},
+        "roofline": {"kernel": "attn_fwd_kernel / attn_bwd_dq_kernel / attn_bwd_dkv_kernel (segmented), "
+                               "slowest rank", "bound": "mfma", "achieved": round(tf, 2), "peak": 157.3,
+                     "unit": "TFLOP/s", "frac": round(tf / 157.3, 4), "traffic": None,
+                     "flops_per_rank": flops},
+        "rank_fwd_ms": [round(x, 3) for x in fwd_ms], "rank_bwd_ms": [round(x, 3) for x in bwd_ms],
+        "rank_tflops": [round(x, 2) for x in tflops],
+        "balance_max_over_min": round(max(rank_ms) / min(rank_ms), 4),
+        "whole_sequence_one_gpu_ms": round(whole_ms, 3),
+        "whole_sequence_over_W_ms": round(whole_ms / W, 3),
+        "rank_mean_ms": round(mean_ms, 3),
+    }
+    print(json.dumps(rec))
+
+
 def main():
     a = parse()
     if a.calibrate_copy:
@@ -149,6 +257,9 @@ def main():
         print(f"bench.py: only --gpus 1 is supported by this build (got {a.gpus}); "
               "the multi-GPU data-parallel exchange is not implemented", file=sys.stderr)
         sys.exit(2)
+    if a.cp:
+        bench_cp(a)
+        return
     import numpy as np
     import torch
 

@@ -573,7 +573,7 @@ __global__ void __launch_bounds__(256) attn_bwd_d_kernel(const float* __restrict
 // SEG: keys and values from sg.kv, dK/dV to sg.dkv (optionally added), queries
 // visible by segment positions; no dS output.
 template <int HDP, bool SEG>
-__global__ void __launch_bounds__(256, 1) attn_bwd_dkv_kernel(
+__global__ void __launch_bounds__(256, (SEG && HDP <= 64) ? 2 : 1) attn_bwd_dkv_kernel(
     const float* __restrict__ dout, const float* __restrict__ qkv, const float* __restrict__ lse,
     const float* __restrict__ Dws, float* __restrict__ dqkv, float* __restrict__ dS, AttnShape sh,
     AttnSegs sg) {
