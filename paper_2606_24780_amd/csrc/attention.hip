@@ -116,6 +116,14 @@ __device__ __forceinline__ void load_rows(floatx4 (&r)[HDP / 32], const float* _
                                           long long stride, int r0, int T, int hd, int tid) {
   constexpr int PER_ROW = HDP / 4;            // float4 per row
   constexpr int ROWS_PER_PASS = 256 / PER_ROW;
+  if (r0 + 32 <= T && hd == HDP) {  // whole tile in range (uniform): no per-element checks
+#pragma unroll
+    for (int i = 0; i < HDP / 32; ++i) {
+      const int row = tid / PER_ROW + ROWS_PER_PASS * i;
+      r[i] = *reinterpret_cast<const floatx4*>(src + (long long)(r0 + row) * stride + 4 * (tid % PER_ROW));
+    }
+    return;
+  }
 #pragma unroll
   for (int i = 0; i < HDP / 32; ++i) {
     const int row = tid / PER_ROW + ROWS_PER_PASS * i;
@@ -368,14 +376,17 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const float* __restric
       zero16(s);
       mma_rows_by_reg<HDP, LDK>(s, sK, qf, lr, hh);
       const int kr0 = key_row(kb);
-      const bool need_mask = (kp0 + 31 > wpos) || (kr0 + 32 > Tk);
+      if ((kp0 + 31 > wpos) || (kr0 + 32 > Tk)) {  // diagonal or ragged tile (uniform)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int kk = acc_row(r, hh);
+          const bool dead = (kp0 + kk > my_qpos) | (kr0 + kk >= Tk);
+          s[r] = dead ? -INFINITY : s[r];
+        }
+      }
       float bmax = -INFINITY;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int kk = acc_row(r, hh);
-        if (need_mask && (kp0 + kk > my_qpos || kr0 + kk >= Tk)) s[r] = -INFINITY;
-        bmax = fmaxf(bmax, s[r]);
-      }
+      for (int r = 0; r < 16; ++r) bmax = fmaxf(bmax, s[r]);
       bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
       const float m_new = fmaxf(m_run, bmax);
       const float alpha = exp2_hw(m_run - m_new);
@@ -516,13 +527,17 @@ __global__ void __launch_bounds__(256, HDP > 64 ? 1 : 2) attn_bwd_dq_kernel(
       mma_rows_by_reg<HDP, LDK>(s, sK, qf, lr, hh);    // S^T  [key][q]
       mma_rows_by_reg<HDP, LDV>(dp, sV, dof, lr, hh);  // dP^T [key][q]
       const int kr0 = key_row(kb);
-      const bool need_mask = (kp0 + 31 > wpos) || (kr0 + 32 > Tk);
+      if ((kp0 + 31 > wpos) || (kr0 + 32 > Tk)) {  // diagonal or ragged tile (uniform)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int kk = acc_row(r, hh);
-        float p = exp2_hw(s[r] - lse2);
-        if (need_mask && (kp0 + kk > my_qpos || kr0 + kk >= Tk)) p = 0.f;
-        s[r] = p * (dp[r] - Dq);  // dS^T
+        for (int r = 0; r < 16; ++r) {
+          const int kk = acc_row(r, hh);
+          const bool dead = (kp0 + kk > my_qpos) | (kr0 + kk >= Tk);
+          const float p = dead ? 0.f : exp2_hw(s[r] - lse2);
+          s[r] = p * (dp[r] - Dq);  // dS^T
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[r] = exp2_hw(s[r] - lse2) * (dp[r] - Dq);
       }
       mma_tile_T_by_acc<HDP, LDK>(dq, sK, s, lr, hh);  // dQ^T[d][q] += K^T dS^T
     }
@@ -573,7 +588,7 @@ __global__ void __launch_bounds__(256) attn_bwd_d_kernel(const float* __restrict
 // SEG: keys and values from sg.kv, dK/dV to sg.dkv (optionally added), queries
 // visible by segment positions; no dS output.
 template <int HDP, bool SEG>
-__global__ void __launch_bounds__(256, (SEG && HDP <= 64) ? 2 : 1) attn_bwd_dkv_kernel(
+__global__ void __launch_bounds__(256, HDP <= 64 ? 2 : 1) attn_bwd_dkv_kernel(
     const float* __restrict__ dout, const float* __restrict__ qkv, const float* __restrict__ lse,
     const float* __restrict__ Dws, float* __restrict__ dqkv, float* __restrict__ dS, AttnShape sh,
     AttnSegs sg) {
@@ -686,22 +701,36 @@ __global__ void __launch_bounds__(256, (SEG && HDP <= 64) ? 2 : 1) attn_bwd_dkv_
       zero16(dp);
       mma_rows_by_reg<HDP, LD>(s, sQ, kf, lr, hh);    // S  [q][key]
       mma_rows_by_reg<HDP, LD>(dp, sdO, vf, lr, hh);  // dP [q][key]
-      const bool need_mask = (qp < kwpos + 31) || (my_k >= Tk);
+      if ((qp < kwpos + 31) || (kw0 + 32 > Tk)) {  // diagonal or ragged tile (uniform)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int qi = acc_row(r, hh);
-        float p = exp2_hw(s[r] - sl[qi]);
-        if (need_mask && (my_kpos > qp + qi || my_k >= Tk)) p = 0.f;
-        s[r] = p;
-        dp[r] = p * (dp[r] - sd[qi]);
+        for (int r = 0; r < 16; ++r) {
+          const int qi = acc_row(r, hh);
+          const bool dead = (my_kpos > qp + qi) | (my_k >= Tk);
+          const float p = dead ? 0.f : exp2_hw(s[r] - sl[qi]);
+          s[r] = p;
+          dp[r] = p * (dp[r] - sd[qi]);
+        }
+      } else {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int qi = acc_row(r, hh);
+          const float p = exp2_hw(s[r] - sl[qi]);
+          s[r] = p;
+          dp[r] = p * (dp[r] - sd[qi]);
+        }
       }
       mma_tile_T_by_acc<HDP, LD>(dv, sdO, s, lr, hh);  // dV^T[d][key] += dO^T P
       mma_tile_T_by_acc<HDP, LD>(dk, sQ, dp, lr, hh);  // dK^T[d][key] += Q^T dS
       if (ds_col && ds_lane) {
+        if (qv0 + 32 <= sh.T) {  // whole query tile in range (uniform)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int q = qv0 + acc_row(r, hh);
-          if (q < sh.T) ds_col[(long long)q * sh.T] = dp[r] * sm_scale;
+          for (int r = 0; r < 16; ++r) ds_col[(long long)(qv0 + acc_row(r, hh)) * sh.T] = dp[r] * sm_scale;
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int q = qv0 + acc_row(r, hh);
+            if (q < sh.T) ds_col[(long long)q * sh.T] = dp[r] * sm_scale;
+          }
         }
       }
     } else if (ds_col && ds_lane && qv0 < kw0) {
