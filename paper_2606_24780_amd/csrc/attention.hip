@@ -701,25 +701,22 @@ __global__ void __launch_bounds__(256, HDP <= 64 ? 2 : 1) attn_bwd_dkv_kernel(
       zero16(dp);
       mma_rows_by_reg<HDP, LD>(s, sQ, kf, lr, hh);    // S  [q][key]
       mma_rows_by_reg<HDP, LD>(dp, sdO, vf, lr, hh);  // dP [q][key]
+      // P needs only S: it is formed while the dP products run, and the dV
+      // products (which need only P) run while dS is formed.
       if ((qp < kwpos + 31) || (kw0 + 32 > Tk)) {  // diagonal or ragged tile (uniform)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int qi = acc_row(r, hh);
           const bool dead = (my_kpos > qp + qi) | (my_k >= Tk);
-          const float p = dead ? 0.f : exp2_hw(s[r] - sl[qi]);
-          s[r] = p;
-          dp[r] = p * (dp[r] - sd[qi]);
+          s[r] = dead ? 0.f : exp2_hw(s[r] - sl[qi]);
         }
       } else {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int qi = acc_row(r, hh);
-          const float p = exp2_hw(s[r] - sl[qi]);
-          s[r] = p;
-          dp[r] = p * (dp[r] - sd[qi]);
-        }
+        for (int r = 0; r < 16; ++r) s[r] = exp2_hw(s[r] - sl[acc_row(r, hh)]);
       }
       mma_tile_T_by_acc<HDP, LD>(dv, sdO, s, lr, hh);  // dV^T[d][key] += dO^T P
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dp[r] = s[r] * (dp[r] - sd[acc_row(r, hh)]);  // dS
       mma_tile_T_by_acc<HDP, LD>(dk, sQ, dp, lr, hh);  // dK^T[d][key] += Q^T dS
       if (ds_col && ds_lane) {
         if (qv0 + 32 <= sh.T) {  // whole query tile in range (uniform)
