@@ -328,6 +328,9 @@ def main():
             k["frac_copy"] = k["gbs"] / copy_gbs
         kernels[name] = k
     traffic, algo_bytes = gemm_traffic()
+    if big or long_ctx or B != 16 or T != 1024:
+        # the committed counters cover the B = 16, T = 1024 step only
+        traffic, algo_bytes = None, None
     roofline = {
         "kernel": "gemm_f32_mfma (all bt_gemm calls of the step, incl. split-K reduction)",
         "bound": "mfma", "achieved": round(gemm_tflops, 3), "peak": MFMA_FP32_PEAK_TFLOPS,
