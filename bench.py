@@ -150,7 +150,9 @@ def bench_cp(a):
     load-balanced two-chunk split.  A step is one rank's forward ring (W
     block forwards, merged) plus its backward ring (row sums, W block
     backwards); every rank is timed, all ranks' tensors resident on the one
-    GPU.  The shard exchange between GPUs is not part of this timing."""
+    GPU.  The backward uses the stored-dS method (the recomputing one is
+    timed beside it).  The shard exchange between GPUs is not part of this
+    timing."""
     import numpy as np
     import torch
 
@@ -172,7 +174,9 @@ def bench_cp(a):
     dq = [torch.empty((B * Tl, 3 * C), device="cuda") for _ in range(W)]
     kv_of = lambda s: (qkv[s][:, C:], 3 * C)
     dkv_of = lambda s: dq[s][:, C:]
-    ring.emulate(W, T, B, H, hd, qkv, out, lse, kv_of, dout=dout, D=D, dqkv=dq, dkv_of=dkv_of)
+    # scratch of the stored-dS backward, shared by every step
+    ws = torch.empty(ring.ws_bytes(W, T, B, H, hd), dtype=torch.uint8, device="cuda")
+    ring.emulate(W, T, B, H, hd, qkv, out, lse, kv_of, dout=dout, D=D, dqkv=dq, dkv_of=dkv_of, ws=ws)
     torch.cuda.synchronize()
 
     def fwd(r):
@@ -180,12 +184,13 @@ def bench_cp(a):
             kv, ks = kv_of(ring.shard_at(r, i, W))
             ring.forward_step(r, i, W, T, B, H, hd, qkv[r], kv, ks, out[r], lse[r])
 
-    def bwd(r):
+    def bwd(r, scratch=ws):
         bt.bt_attention_rowdot(dout[r], out[r], D[r], B, Tl, H, hd)
         for i in range(W):
             s_ = ring.shard_at(r, i, W)
             kv, ks = kv_of(s_)
-            ring.backward_step(r, i, W, T, B, H, hd, dout[r], qkv[r], kv, ks, lse[r], D[r], dq[r], dkv_of(s_))
+            ring.backward_step(r, i, W, T, B, H, hd, dout[r], qkv[r], kv, ks, lse[r], D[r], dq[r], dkv_of(s_),
+                               scratch)
 
     def timed(fn, reps):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -203,6 +208,8 @@ def bench_cp(a):
     torch.cuda.synchronize()
     fwd_ms = [timed(lambda: fwd(r), a.steps) for r in range(W)]
     bwd_ms = [timed(lambda: bwd(r), a.steps) for r in range(W)]
+    bwd_recompute_ms = [timed(lambda: bwd(r, None), a.steps) for r in range(W)]
+    del ws
     rank_ms = [f + b for f, b in zip(fwd_ms, bwd_ms)]
     # credited work: 4 hd FLOP per visible (query, key) pair forward, 8 hd
     # backward; the split gives every rank 1/W of the T (T + 1) / 2 pairs
@@ -239,6 +246,7 @@ def bench_cp(a):
                      "unit": "TFLOP/s", "frac": round(tf / 157.3, 4), "traffic": None,
                      "flops_per_rank": flops},
         "rank_fwd_ms": [round(x, 3) for x in fwd_ms], "rank_bwd_ms": [round(x, 3) for x in bwd_ms],
+        "rank_bwd_recompute_ms": [round(x, 3) for x in bwd_recompute_ms],
         "rank_tflops": [round(x, 2) for x in tflops],
         "balance_max_over_min": round(max(rank_ms) / min(rank_ms), 4),
         "whole_sequence_one_gpu_ms": round(whole_ms, 3),

@@ -217,13 +217,24 @@ bt_status bt_attention_rowdot(const float* dout, const float* out, float* D, int
  * dQ goes to the Q part of dqkv [B, Tq, 3, H, hd] (its K and V parts are not
  * touched); dK and dV of the shard go to dkv, laid out as kv (same
  * kv_stride).  accumulate: bit 0 adds into dQ, bit 1 adds into dK/dV (else
- * they are overwritten).  Deterministic; no workspace.  Errors as
- * bt_attention_block_fwd; gradients must not alias inputs (BT_EINVAL).
+ * they are overwritten).  Deterministic.
+ * ws (16-byte aligned, caller-owned scratch) selects the method:
+ *  - ws_bytes >= bt_attention_block_bwd_ws_bytes() > 0: a key-major pass
+ *    (dK, dV) that also stores dS / sqrt(hd) ([B, H, Tq, Tk] floats in ws),
+ *    then dQ (+)= dS K as one batched matrix-core product over the visible
+ *    key range of each 128-row tile.  Needs every segment position to be a
+ *    multiple of 128 (the load-balanced split's are); otherwise the size
+ *    function returns 0.
+ *  - otherwise (ws may be NULL): a query-major pass recomputes S and dP for
+ *    dQ and the key-major pass gives dK, dV; no workspace.
+ * Errors as bt_attention_block_fwd; gradients must not alias inputs
+ * (BT_EINVAL).
  */
 bt_status bt_attention_block_bwd(const float* dout, const float* qkv, const float* kv, long long kv_stride,
                                  const float* lse, const float* D, float* dqkv, float* dkv,
-                                 int accumulate, int B, int H, int hd, const bt_cp_segments* segs,
-                                 void* stream);
+                                 int accumulate, void* ws, size_t ws_bytes, int B, int H, int hd,
+                                 const bt_cp_segments* segs, void* stream);
+size_t bt_attention_block_bwd_ws_bytes(int B, int H, int hd, const bt_cp_segments* segs);
 
 /*
  * LayerNorm forward over the last dimension (pre-normalised blocks of the

@@ -90,8 +90,9 @@ _SIGS = {
     "bt_attention_block_fwd": (i32, [vp, vp, i64, vp, vp, i32, i32, i32, i32, _c.POINTER(CPSegments), vp]),
     "bt_attention_lse_merge": (i32, [vp, vp, vp, vp, i32, i32, i32, i32, vp]),
     "bt_attention_rowdot": (i32, [vp, vp, vp, i32, i32, i32, i32, vp]),
-    "bt_attention_block_bwd": (i32, [vp, vp, vp, i64, vp, vp, vp, vp, i32, i32, i32, i32,
+    "bt_attention_block_bwd": (i32, [vp, vp, vp, i64, vp, vp, vp, vp, i32, vp, sz, i32, i32, i32,
                                      _c.POINTER(CPSegments), vp]),
+    "bt_attention_block_bwd_ws_bytes": (sz, [i32, i32, i32, _c.POINTER(CPSegments)]),
     "bt_layernorm_fwd": (i32, [vp, vp, vp, vp, vp, vp, i32, i32, f32, vp]),
     "bt_layernorm_bwd": (i32, [vp, vp, vp, vp, vp, vp, vp, vp, f32, f32, vp, sz, i32, i32, vp]),
     "bt_layernorm_bwd_ws_bytes": (sz, [i32, i32]),
@@ -246,10 +247,17 @@ def bt_attention_rowdot(dout, out, D, B, T, H, hd, stream=None):
 
 
 def bt_attention_block_bwd(dout, qkv, kv, kv_stride, lse, D, dqkv, dkv, accumulate, B, H, hd, segs,
-                           stream=None):
+                           ws=None, stream=None):
+    """ws: a uint8 tensor of at least bt_attention_block_bwd_ws_bytes() selects
+    the stored-dS method; None, the recomputing one."""
+    nbytes = 0 if ws is None else ws.numel() * ws.element_size()
     _check(lib().bt_attention_block_bwd(_p(dout), _p(qkv), _p(kv), kv_stride, _p(lse), _p(D), _p(dqkv),
-                                        _p(dkv), int(accumulate), B, H, hd, _c.byref(segs),
+                                        _p(dkv), int(accumulate), _p(ws), nbytes, B, H, hd, _c.byref(segs),
                                         _stream(stream)), "bt_attention_block_bwd")
+
+
+def bt_attention_block_bwd_ws_bytes(B, H, hd, segs) -> int:
+    return lib().bt_attention_block_bwd_ws_bytes(B, H, hd, _c.byref(segs))
 
 
 def bt_layernorm_fwd(x, gamma, beta, y, mean, rstd, M, C, eps=1e-5, stream=None):

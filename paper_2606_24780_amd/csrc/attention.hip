@@ -586,7 +586,8 @@ __global__ void __launch_bounds__(256) attn_bwd_d_kernel(const float* __restrict
 
 // ------------------------------------------------ backward: dK and dV (key-major)
 // SEG: keys and values from sg.kv, dK/dV to sg.dkv (optionally added), queries
-// visible by segment positions; no dS output.
+// visible by segment positions; dS ([B, H, T, Tk]) when positions are
+// multiples of 128 (the segmented dQ product's tiles).
 template <int HDP, bool SEG>
 __global__ void __launch_bounds__(256, HDP <= 64 ? 2 : 1) attn_bwd_dkv_kernel(
     const float* __restrict__ dout, const float* __restrict__ qkv, const float* __restrict__ lse,
@@ -622,9 +623,9 @@ __global__ void __launch_bounds__(256, HDP <= 64 ? 2 : 1) attn_bwd_dkv_kernel(
   const int kwpos = kp0 + 32 * wave;
   const int my_kpos = kwpos + lr;
   const float sm_scale = 1.f / sqrtf((float)sh.hd);
-  // dS / sqrt(hd) for the dQ product, [B, H, T, T], column my_k of this lane
-  float* ds_col = (!SEG && dS) ? dS + (long long)bh * sh.T * sh.T + my_k : nullptr;
-  const bool ds_lane = my_k < sh.T;
+  // dS / sqrt(hd) for the dQ product, [B, H, T, Tk], column my_k of this lane
+  float* ds_col = dS ? dS + (long long)bh * sh.T * Tk + my_k : nullptr;
+  const bool ds_lane = my_k < Tk;
 
   float kf[HDP / 2], vf[HDP / 2];
   load_reg_operand<HDP>(kf, kbase, ks, my_k, Tk, sh.hd, hh, LOG2E * sm_scale);
@@ -721,23 +722,23 @@ __global__ void __launch_bounds__(256, HDP <= 64 ? 2 : 1) attn_bwd_dkv_kernel(
       if (ds_col && ds_lane) {
         if (qv0 + 32 <= sh.T) {  // whole query tile in range (uniform)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) ds_col[(long long)(qv0 + acc_row(r, hh)) * sh.T] = dp[r] * sm_scale;
+          for (int r = 0; r < 16; ++r) ds_col[(long long)(qv0 + acc_row(r, hh)) * Tk] = dp[r] * sm_scale;
         } else {
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int q = qv0 + acc_row(r, hh);
-            if (q < sh.T) ds_col[(long long)q * sh.T] = dp[r] * sm_scale;
+            if (q < sh.T) ds_col[(long long)q * Tk] = dp[r] * sm_scale;
           }
         }
       }
-    } else if (ds_col && ds_lane && qv0 < kw0) {
+    } else if (ds_col && ds_lane && qp < kwpos) {
       // query tiles of the diagonal 128-row tile that precede this wave's
       // keys: fully masked, stored as zeros because the dQ product of that
       // tile sums keys up to the tile's end
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int q = qv0 + acc_row(r, hh);
-        if (q < sh.T) ds_col[(long long)q * sh.T] = 0.f;
+        if (q < sh.T) ds_col[(long long)q * Tk] = 0.f;
       }
     }
     if (more) store_q(smem + (cur ^ 1) * BUF);
@@ -1025,26 +1026,57 @@ extern "C" bt_status bt_attention_rowdot(const float* dout, const float* out, fl
   return launch_d(dout, out, D, B, T, H, hd, as_stream(stream));
 }
 
+// The stored-dS method of a ring step: needs positions that are multiples of
+// 128 (the dQ product's row tiles then meet the key tiles on their edges).
+static bool block_stores_ds(const bt_cp_segments* g) {
+  for (int i = 0; i < g->n_q; ++i)
+    if (g->q_pos[i] % 128) return false;
+  for (int i = 0; i < g->n_k; ++i)
+    if (g->k_pos[i] % 128) return false;
+  return true;
+}
+
+extern "C" size_t bt_attention_block_bwd_ws_bytes(int B, int H, int hd, const bt_cp_segments* segs) {
+  (void)hd;
+  if (!segs || B <= 0 || H <= 0 || segs->seg <= 0 || segs->n_q < 1 || segs->n_q > 2 || segs->n_k < 1 ||
+      segs->n_k > 2 || !block_stores_ds(segs))
+    return 0;
+  return align_up((size_t)B * H * segs->n_q * segs->seg * segs->n_k * segs->seg * sizeof(float), 256);
+}
+
 extern "C" bt_status bt_attention_block_bwd(const float* dout, const float* qkv, const float* kv, long long kv_stride,
                                             const float* lse, const float* D, float* dqkv, float* dkv,
-                                            int accumulate, int B, int H, int hd, const bt_cp_segments* segs,
-                                            void* stream) {
+                                            int accumulate, void* ws, size_t ws_bytes, int B, int H, int hd,
+                                            const bt_cp_segments* segs, void* stream) {
   AttnSegs sg;
   int Tq = 0;
   BT_TRY(make_segs(segs, H, hd, kv, dkv, kv_stride, &sg, &Tq, "bt_attention_block_bwd"));
   BT_TRY(check_attn(qkv, dout, B, Tq, H, hd, "bt_attention_block_bwd"));
   BT_TRY(check_attn(kv, dout, B, sg.Tk, H, hd, "bt_attention_block_bwd"));
   BT_RETURN_IF(!lse || !D || !dqkv || !dkv, BT_EINVAL, "bt_attention_block_bwd: NULL pointer");
-  BT_RETURN_IF(!aligned16(qkv) || !aligned16(dout) || !aligned16(dqkv), BT_EALIGN,
-               "bt_attention_block_bwd: tensors must be 16-byte aligned");
+  BT_RETURN_IF(!aligned16(qkv) || !aligned16(dout) || !aligned16(dqkv) || (ws && !aligned16(ws)), BT_EALIGN,
+               "bt_attention_block_bwd: tensors and workspace must be 16-byte aligned");
   BT_RETURN_IF(accumulate < 0 || accumulate > 3, BT_EINVAL, "bt_attention_block_bwd: accumulate must be 0..3");
   BT_RETURN_IF(dqkv == qkv || dkv == kv, BT_EINVAL, "bt_attention_block_bwd: gradients must not alias inputs");
   sg.flags = accumulate;
   AttnShape sh{B, Tq, H, hd, 3LL * H * hd};
   hipStream_t s = as_stream(stream);
+  const size_t need = bt_attention_block_bwd_ws_bytes(B, H, hd, segs);
+  const dim3 gk((unsigned)(B * H * (sg.Tk / 128)));
+  if (need && ws && ws_bytes >= need) {
+    // key-major pass with dS stored, then dQ (+)= dS K over the visible key
+    // ranges of each 128-row tile on the matrix-core GEMM
+    float* dS = static_cast<float*>(ws);
+    launch_dkv<true>(hd, gk, s, dout, qkv, lse, D, nullptr, dS, sh, sg);
+    BT_TRY(check_launch("attn_bwd_dkv_kernel (block, dS)"));
+    const long long rs = sh.row_stride, ks = kv_stride, Tk = sg.Tk;
+    return gemm_segmented_batched(Tq, hd, sg.Tk, dS, sg.Tk, (long long)H * Tq * Tk, (long long)Tq * Tk, kv, (int)ks,
+                                  Tk * ks, hd, dqkv, (int)rs, (long long)Tq * rs, hd, B, H,
+                                  (accumulate & SEG_ACC_DQ) ? 1.f : 0.f, sg.seg, sg.q_pos, sg.k_pos, s);
+  }
   launch_dq<true>(hd, dim3((unsigned)(B * H * (Tq / 128))), s, dout, qkv, nullptr, lse, dqkv,
                   const_cast<float*>(D), sh, sg);
   BT_TRY(check_launch("attn_bwd_dq_kernel (block)"));
-  launch_dkv<true>(hd, dim3((unsigned)(B * H * (sg.Tk / 128))), s, dout, qkv, lse, D, nullptr, nullptr, sh, sg);
+  launch_dkv<true>(hd, gk, s, dout, qkv, lse, D, nullptr, nullptr, sh, sg);
   return check_launch("attn_bwd_dkv_kernel (block)");
 }

@@ -42,6 +42,14 @@ bt_status sum_partials(const float* part, int nb, long long ld, int n, float* ou
 bt_status gemm_causal_batched(int M, int N, int K, const float* A, int lda, long long sa_b, long long sa_h,
                               const float* B, int ldb, long long sb_b, long long sb_h, float* C, int ldc,
                               long long sc_b, long long sc_h, int nb, int nh, hipStream_t stream);
+// Segmented variant (context-parallel attention): rows of A and C are 1 or 2
+// segments of `seg` rows at positions q_pos[], the K range 1 or 2 segments at
+// k_pos[] (seg and positions multiples of 128); row tile sums the k whose
+// positions do not exceed its last row's.  C = product + beta C, beta 0 or 1.
+bt_status gemm_segmented_batched(int M, int N, int K, const float* A, int lda, long long sa_b, long long sa_h,
+                                 const float* B, int ldb, long long sb_b, long long sb_h, float* C, int ldc,
+                                 long long sc_b, long long sc_h, int nb, int nh, float beta, int seg,
+                                 const int* q_pos, const int* k_pos, hipStream_t stream);
 
 // ------------------------------------------------------------------ device
 typedef float floatx4 __attribute__((ext_vector_type(4)));

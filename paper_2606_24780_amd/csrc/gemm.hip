@@ -67,10 +67,16 @@ struct GemmParams {
   int splits;
   int tiles_m, tiles_n;
   float beta;
-  // batched causal products only: batch y addresses A + (y / batch_h) sa_b +
+  // batched products only: batch y addresses A + (y / batch_h) sa_b +
   // (y % batch_h) sa_h (likewise B, C)
   int nbatch, batch_h;
   long long sa_b, sa_h, sb_b, sb_h, sc_b, sc_h;
+  // segmented batched products only: rows of A (and C) are 1 or 2 segments
+  // of `seg` rows starting at positions q_pos[i], the K range 1 or 2 such
+  // segments at k_pos[i]; output row i sums the k whose position is at most
+  // the last position of its BM-row tile
+  int seg;
+  int q_pos[2], k_pos[2];
 };
 
 // LDS floats of one R-row operand tile: K-contiguous [R][BK] (swizzled) or
@@ -275,13 +281,16 @@ __device__ __forceinline__ void epilogue_block(const GemmParams& p, const floatx
 // full (M, N multiples of the block tile, K range a multiple of BK), and
 // operand tiles are copied straight from global memory into LDS; otherwise
 // they are staged through registers with bounds checks (ragged shapes).
-// CAUSAL: a batch of products (blockIdx.x % nbatch selects the batch) in
-// which the output rows of a tile starting at m0 only sum k < m0 + BM; tile
-// rows are launched heaviest first.  OCC is the number of waves per SIMD the
+// BMODE 1 (causal): a batch of products (blockIdx.x % nbatch selects the
+// batch) in which the output rows of a tile starting at m0 only sum
+// k < m0 + BM; tile rows are launched heaviest first.  BMODE 2 (segmented):
+// the same with positions (GemmParams::seg): a row tile sums, in each key
+// segment, the prefix of k whose positions do not exceed its last row's, in
+// BM-aligned steps.  OCC is the number of waves per SIMD the
 // register allocation must allow (the second launch-bounds argument on
 // AMDGPU); a CU then holds 4 OCC / (WM WN) blocks.
 template <bool A_KC, bool B_KC, int EPI, bool SPLIT, bool COLSUM, int BK, int OCC, int WM, int WN, int MB, int NB,
-          bool DTL, bool CAUSAL>
+          bool DTL, int BMODE>
 __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmParams pk) {
   GemmParams p = pk;
   constexpr int WTM = 32 * MB, WTN = 32 * NB;  // wave tile: MB x NB MFMA 32x32 blocks
@@ -307,7 +316,7 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
   const int wm = wave / WN, wn = wave % WN;
 
   int z, tm, tn;
-  if (CAUSAL) {
+  if (BMODE != 0) {
     const int y = blockIdx.x % p.nbatch;
     const int rank = blockIdx.x / p.nbatch;  // 0: last tile row (longest k range)
     tm = p.tiles_m - 1 - rank / p.tiles_n;
@@ -337,8 +346,18 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
 
   const int kbeg = z * p.ksplit;
   int kend = min(p.K, kbeg + p.ksplit);
-  if (CAUSAL) kend = min(kend, m0 + BM);
-  const int nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+  if (BMODE == 1) kend = min(kend, m0 + BM);
+  int nk, n0t = 0;  // k-tiles; segmented: k-tiles in the first key segment
+  if (BMODE == 2) {
+    const int last = (m0 < p.seg ? p.q_pos[0] + m0 : p.q_pos[1] + (m0 - p.seg)) + BM - 1;
+    auto visible = [&](int kpos) { return last < kpos ? 0 : min(p.seg, (last - kpos) / BM * BM + BM); };
+    n0t = visible(p.k_pos[0]) / BK;
+    nk = n0t + (p.K > p.seg ? visible(p.k_pos[1]) / BK : 0);
+  } else {
+    nk = kend > kbeg ? (kend - kbeg + BK - 1) / BK : 0;
+  }
+  // k offset (from kbeg) of k-tile t
+  auto koff = [&](int t) { return BMODE == 2 ? (t < n0t ? t * BK : p.seg + (t - n0t) * BK) : t * BK; };
 
   floatx16 acc[MB][NB];
 #pragma unroll
@@ -351,8 +370,8 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
   floatx4 ra[NVA], rb[NVB];
   const float* ga[CA];
   const float* gb[CB];
-  const long long a_step = A_KC ? BK : (long long)BK * p.lda;  // per k-tile source advance
-  const long long b_step = B_KC ? BK : (long long)BK * p.ldb;
+  const long long a_unit = A_KC ? 1 : p.lda;  // source advance per unit of k
+  const long long b_unit = B_KC ? 1 : p.ldb;
   // Column sums of op(B) (only for MN-contiguous B, i.e. op(B) = B [K][N]),
   // kept only by the first tile row of blocks (tm == 0).  Staged path: each
   // thread adds up the B rows it stages and the NT / (BN/4) row groups are
@@ -369,12 +388,12 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
   }
   if (nk > 0) {
     if (DTL) {
-      copy_issue<CA>(ga, 0, smem, wave);
-      copy_issue<CB>(gb, 0, smem + A_SZ, wave);
+      copy_issue<CA>(ga, koff(0) * a_unit, smem, wave);
+      copy_issue<CB>(gb, koff(0) * b_unit, smem + A_SZ, wave);
       wait_copies();
     } else {
-      load_tile<A_KC, BM, BK, NT>(ra, p.A, p.lda, m0, p.M, kbeg, kend, tid);
-      load_tile<B_KC, BN, BK, NT>(rb, p.B, p.ldb, n0, p.N, kbeg, kend, tid);
+      load_tile<A_KC, BM, BK, NT>(ra, p.A, p.lda, m0, p.M, kbeg + koff(0), kend, tid);
+      load_tile<B_KC, BN, BK, NT>(rb, p.B, p.ldb, n0, p.N, kbeg + koff(0), kend, tid);
       if (COLSUM)
 #pragma unroll
         for (int i = 0; i < NVB; ++i) csum += rb[i];
@@ -391,10 +410,10 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
       if (DTL) {
         // the other buffer was last read before the previous barrier
         float* sN = smem + (cur ^ 1) * (A_SZ + B_SZ);
-        copy_issue<CA>(ga, (kt + 1) * a_step, sN, wave);
-        copy_issue<CB>(gb, (kt + 1) * b_step, sN + A_SZ, wave);
+        copy_issue<CA>(ga, koff(kt + 1) * a_unit, sN, wave);
+        copy_issue<CB>(gb, koff(kt + 1) * b_unit, sN + A_SZ, wave);
       } else {
-        const int k0 = kbeg + (kt + 1) * BK;
+        const int k0 = kbeg + koff(kt + 1);
         load_tile<A_KC, BM, BK, NT>(ra, p.A, p.lda, m0, p.M, k0, kend, tid);
         load_tile<B_KC, BN, BK, NT>(rb, p.B, p.ldb, n0, p.N, k0, kend, tid);
       }
@@ -607,26 +626,26 @@ void launch_cfg(const GemmParams& p, int epi, bool split, dim3 grid, hipStream_t
   const dim3 block(64 * WM * WN);
   if (split) {
     if (cs)
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, !B_KC, BK, OCC, WM, WN, MB, NB, DTL, false>), grid, block, 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, !B_KC, BK, OCC, WM, WN, MB, NB, DTL, 0>), grid, block, 0, s, p);
     else
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, false, BK, OCC, WM, WN, MB, NB, DTL, false>), grid, block, 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, true, false, BK, OCC, WM, WN, MB, NB, DTL, 0>), grid, block, 0, s, p);
     return;
   }
   switch (epi) {
     case BT_EPI_NONE:
       if (cs)
-        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, !B_KC, BK, OCC, WM, WN, MB, NB, DTL, false>), grid, block, 0, s, p);
+        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, !B_KC, BK, OCC, WM, WN, MB, NB, DTL, 0>), grid, block, 0, s, p);
       else
-        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, false, BK, OCC, WM, WN, MB, NB, DTL, false>), grid, block, 0, s, p);
+        hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_NONE, false, false, BK, OCC, WM, WN, MB, NB, DTL, 0>), grid, block, 0, s, p);
       break;
     case BT_EPI_BIAS:
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS, false, false, BK, OCC, WM, WN, MB, NB, DTL, false>), grid, block, 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS, false, false, BK, OCC, WM, WN, MB, NB, DTL, 0>), grid, block, 0, s, p);
       break;
     case BT_EPI_BIAS_GELU:
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS_GELU, false, false, BK, OCC, WM, WN, MB, NB, DTL, false>), grid, block, 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_BIAS_GELU, false, false, BK, OCC, WM, WN, MB, NB, DTL, 0>), grid, block, 0, s, p);
       break;
     default:
-      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_DGELU, false, false, BK, OCC, WM, WN, MB, NB, DTL, false>), grid, block, 0, s, p);
+      hipLaunchKernelGGL((gemm_f32_mfma<A_KC, B_KC, BT_EPI_DGELU, false, false, BK, OCC, WM, WN, MB, NB, DTL, 0>), grid, block, 0, s, p);
       break;
   }
 }
@@ -647,60 +666,94 @@ void launch_layout(const GemmParams& p, const GemmCfg& c, int epi, bool split, b
 
 }  // namespace
 
-// One configuration of the batched causal product: a (32 MB WM) x (32 NB WN)
-// block tile of WM x WN waves, each wave a (32 MB) x (32 NB) tile.
-template <int WM, int WN, int MB, int NB, int OCC>
-static bt_status launch_causal(GemmParams p, hipStream_t stream) {
+// One configuration of the batched causal / segmented product: a
+// (32 MB WM) x (32 NB WN) block tile of WM x WN waves, each wave a
+// (32 MB) x (32 NB) tile.
+template <int BMODE, int WM, int WN, int MB, int NB, int OCC>
+static bt_status launch_batched(GemmParams p, hipStream_t stream) {
   constexpr int BK = 16, BM = 32 * MB * WM, BN = 32 * NB * WN;
   p.ksplit = (p.K + BK - 1) / BK * BK;
   p.splits = 1;
   p.tiles_m = (p.M + BM - 1) / BM;
   p.tiles_n = (p.N + BN - 1) / BN;
   const long long nblocks = (long long)p.tiles_m * p.tiles_n * p.nbatch;
-  BT_RETURN_IF(nblocks > 0x7fffffffLL, BT_ESHAPE, "gemm_causal_batched: too many tiles");
+  BT_RETURN_IF(nblocks > 0x7fffffffLL, BT_ESHAPE, "batched product: too many tiles");
   const bool dtl = p.M % BM == 0 && p.N % BN == 0 && p.K % BK == 0;
   if (dtl)
-    hipLaunchKernelGGL((gemm_f32_mfma<true, false, BT_EPI_NONE, false, false, BK, OCC, WM, WN, MB, NB, true, true>),
+    hipLaunchKernelGGL((gemm_f32_mfma<true, false, BT_EPI_NONE, false, false, BK, OCC, WM, WN, MB, NB, true, BMODE>),
                        dim3((unsigned)nblocks), dim3(64 * WM * WN), 0, stream, p);
   else
-    hipLaunchKernelGGL((gemm_f32_mfma<true, false, BT_EPI_NONE, false, false, BK, OCC, WM, WN, MB, NB, false, true>),
+    hipLaunchKernelGGL((gemm_f32_mfma<true, false, BT_EPI_NONE, false, false, BK, OCC, WM, WN, MB, NB, false, BMODE>),
                        dim3((unsigned)nblocks), dim3(64 * WM * WN), 0, stream, p);
-  return check_launch("gemm_f32_mfma (batched causal)");
+  return check_launch(BMODE == 1 ? "gemm_f32_mfma (batched causal)" : "gemm_f32_mfma (batched segmented)");
+}
+
+static bt_status batched_params(GemmParams* p, const char* who, int M, int N, int K, const float* A, int lda,
+                                long long sa_b, long long sa_h, const float* B, int ldb, long long sb_b,
+                                long long sb_h, float* C, int ldc, long long sc_b, long long sc_h, int nb,
+                                int nh) {
+  BT_RETURN_IF(M <= 0 || N <= 0 || K <= 0 || nb <= 0 || nh <= 0, BT_ESHAPE,
+               "%s: bad sizes M=%d N=%d K=%d nb=%d nh=%d", who, M, N, K, nb, nh);
+  BT_RETURN_IF((M | N | K | lda | ldb | ldc) & 3, BT_ESHAPE, "%s: sizes and strides must be multiples of 4", who);
+  BT_RETURN_IF(!aligned16(A) || !aligned16(B) || !aligned16(C) || ((sa_b | sa_h | sb_b | sb_h | sc_b | sc_h) & 3),
+               BT_EALIGN, "%s: operands must be 16-byte aligned", who);
+  *p = GemmParams{};
+  p->A = A;
+  p->B = B;
+  p->C = C;
+  p->lda = lda;
+  p->ldb = ldb;
+  p->ldc = ldc;
+  p->M = M;
+  p->N = N;
+  p->K = K;
+  p->nbatch = nb * nh;
+  p->batch_h = nh;
+  p->sa_b = sa_b;
+  p->sa_h = sa_h;
+  p->sb_b = sb_b;
+  p->sb_h = sb_h;
+  p->sc_b = sc_b;
+  p->sc_h = sc_h;
+  return BT_OK;
 }
 
 bt_status gemm_causal_batched(int M, int N, int K, const float* A, int lda, long long sa_b, long long sa_h,
                               const float* B, int ldb, long long sb_b, long long sb_h, float* C, int ldc,
                               long long sc_b, long long sc_h, int nb, int nh, hipStream_t stream) {
-  BT_RETURN_IF(M <= 0 || N <= 0 || K <= 0 || nb <= 0 || nh <= 0, BT_ESHAPE,
-               "gemm_causal_batched: bad sizes M=%d N=%d K=%d nb=%d nh=%d", M, N, K, nb, nh);
-  BT_RETURN_IF((M | N | K | lda | ldb | ldc) & 3, BT_ESHAPE, "gemm_causal_batched: sizes and strides must be multiples of 4");
-  BT_RETURN_IF(!aligned16(A) || !aligned16(B) || !aligned16(C) || ((sa_b | sa_h | sb_b | sb_h | sc_b | sc_h) & 3),
-               BT_EALIGN, "gemm_causal_batched: operands must be 16-byte aligned");
-  GemmParams p{};
-  p.A = A;
-  p.B = B;
-  p.C = C;
-  p.lda = lda;
-  p.ldb = ldb;
-  p.ldc = ldc;
-  p.M = M;
-  p.N = N;
-  p.K = K;
-  p.nbatch = nb * nh;
-  p.batch_h = nh;
-  p.sa_b = sa_b;
-  p.sa_h = sa_h;
-  p.sb_b = sb_b;
-  p.sb_h = sb_h;
-  p.sc_b = sc_b;
-  p.sc_h = sc_h;
+  GemmParams p;
+  BT_TRY(batched_params(&p, "gemm_causal_batched", M, N, K, A, lda, sa_b, sa_h, B, ldb, sb_b, sb_h, C, ldc, sc_b,
+                        sc_h, nb, nh));
   // Both use 128 x 64 block tiles.  Up to T = 8192 rows, four waves of 64 x 32
   // (one wave per SIMD guaranteed, so the register budget is the full file)
   // hide latency better: measured 8-14% faster on MI355X at T = 1024 and
   // 4096.  At T = 16384 each tile's K loop is long enough that two waves of
   // 64 x 64, with their higher arithmetic intensity per LDS read, win by ~1%.
-  if (M <= 8192) return launch_causal<2, 2, 2, 1, 1>(p, stream);
-  return launch_causal<2, 1, 2, 2, 2>(p, stream);
+  if (M <= 8192) return launch_batched<1, 2, 2, 2, 1, 1>(p, stream);
+  return launch_batched<1, 2, 1, 2, 2, 2>(p, stream);
+}
+
+bt_status gemm_segmented_batched(int M, int N, int K, const float* A, int lda, long long sa_b, long long sa_h,
+                                 const float* B, int ldb, long long sb_b, long long sb_h, float* C, int ldc,
+                                 long long sc_b, long long sc_h, int nb, int nh, float beta, int seg,
+                                 const int* q_pos, const int* k_pos, hipStream_t stream) {
+  GemmParams p;
+  BT_TRY(batched_params(&p, "gemm_segmented_batched", M, N, K, A, lda, sa_b, sa_h, B, ldb, sb_b, sb_h, C, ldc,
+                        sc_b, sc_h, nb, nh));
+  constexpr int BM = 128;  // row tile of both configurations below
+  BT_RETURN_IF(seg <= 0 || seg % BM || M % seg || K % seg || M / seg > 2 || K / seg > 2, BT_ESHAPE,
+               "gemm_segmented_batched: segments of %d rows must be multiples of %d and 1 or 2 per side", seg, BM);
+  for (int i = 0; i < 2; ++i) {
+    BT_RETURN_IF(i < M / seg && (q_pos[i] < 0 || q_pos[i] % BM), BT_ESHAPE, "gemm_segmented_batched: bad position");
+    BT_RETURN_IF(i < K / seg && (k_pos[i] < 0 || k_pos[i] % BM), BT_ESHAPE, "gemm_segmented_batched: bad position");
+    p.q_pos[i] = i < M / seg ? q_pos[i] : 0;
+    p.k_pos[i] = i < K / seg ? k_pos[i] : 0;
+  }
+  BT_RETURN_IF(beta != 0.f && beta != 1.f, BT_EINVAL, "gemm_segmented_batched: beta must be 0 or 1");
+  p.seg = seg;
+  p.beta = beta;
+  if (M <= 8192) return launch_batched<2, 2, 2, 2, 1, 1>(p, stream);
+  return launch_batched<2, 2, 1, 2, 2, 2>(p, stream);
 }
 
 }  // namespace bt

@@ -35,18 +35,29 @@ def forward_step(rank, step, W, T, B, H, hd, qkv, kv, kv_stride, out, lse, strea
     bt.bt_attention_block_fwd(qkv, kv, kv_stride, out, lse, step > 0, B, H, hd, segs, stream)
 
 
-def backward_step(rank, step, W, T, B, H, hd, dout, qkv, kv, kv_stride, lse, D, dqkv, dkv, stream=None):
+def backward_step(rank, step, W, T, B, H, hd, dout, qkv, kv, kv_stride, lse, D, dqkv, dkv, ws=None,
+                  stream=None):
     """One rank's backward at one ring step: dQ into dqkv (the rank's), dK/dV
-    into dkv (the gradient travelling with the shard)."""
+    into dkv (the gradient travelling with the shard).  ws: scratch for the
+    stored-dS method (see ws_bytes), or None to recompute."""
     segs = bt.bt_cp_rank_segments(T, W, rank, shard_at(rank, step, W))
     acc = 3 if step > 0 else 0
-    bt.bt_attention_block_bwd(dout, qkv, kv, kv_stride, lse, D, dqkv, dkv, acc, B, H, hd, segs, stream)
+    bt.bt_attention_block_bwd(dout, qkv, kv, kv_stride, lse, D, dqkv, dkv, acc, B, H, hd, segs, ws=ws,
+                              stream=stream)
 
 
-def emulate(W, T, B, H, hd, qkv, out, lse, kv_of, dout=None, D=None, dqkv=None, dkv_of=None, stream=None):
+def ws_bytes(W, T, B, H, hd):
+    """Scratch for the stored-dS backward of any step of the ring (every
+    step of the load-balanced split has the same shape)."""
+    return bt.bt_attention_block_bwd_ws_bytes(B, H, hd, bt.bt_cp_rank_segments(T, W, 0, 0))
+
+
+def emulate(W, T, B, H, hd, qkv, out, lse, kv_of, dout=None, D=None, dqkv=None, dkv_of=None, ws=None,
+            stream=None):
     """All W ranks on one GPU.  qkv, out, lse, dout, D, dqkv: per-rank lists
     (local rows, [B, T/W, ...]); kv_of(s) -> (tensor or pointer, stride) of
-    shard s; dkv_of(s) -> its gradient buffer.  Runs the forward ring, and the
+    shard s; dkv_of(s) -> its gradient buffer; ws: scratch for the stored-dS
+    backward (reused by every step), or None.  Runs the forward ring, and the
     backward ring when dout is given."""
     Tl = T // W
     for i in range(W):
@@ -61,4 +72,5 @@ def emulate(W, T, B, H, hd, qkv, out, lse, kv_of, dout=None, D=None, dqkv=None, 
         for r in range(W):
             s = shard_at(r, i, W)
             kv, ks = kv_of(s)
-            backward_step(r, i, W, T, B, H, hd, dout[r], qkv[r], kv, ks, lse[r], D[r], dqkv[r], dkv_of(s), stream)
+            backward_step(r, i, W, T, B, H, hd, dout[r], qkv[r], kv, ks, lse[r], D[r], dqkv[r], dkv_of(s), ws,
+                          stream)

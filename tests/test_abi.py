@@ -162,12 +162,20 @@ def test_cp_block_validation(lib):
     assert fwd(None) == BT_EINVAL
     assert lib.bt_attention_block_fwd(FAKE, FAKE_MIS, 2 * H * hd, FAKE + 131072, FAKE + 196608, 0, 1, H, hd,
                                       segs(), None) == BT_EALIGN
-    bwd = lambda g, acc=0, dkv=FAKE + 262144: lib.bt_attention_block_bwd(
+    bwd = lambda g, acc=0, dkv=FAKE + 262144, ws=None: lib.bt_attention_block_bwd(
         FAKE, FAKE + 65536, FAKE + 131072, 2 * H * hd, FAKE + 196608, FAKE + 200000, FAKE + 327680, dkv, acc,
-        1, H, hd, g, None)
+        ws, 1 << 30, 1, H, hd, g, None)
     assert bwd(segs(), acc=4) == BT_EINVAL
     assert bwd(segs(), dkv=FAKE + 131072) == BT_EINVAL    # dkv aliases kv
     assert bwd(segs(seg=64)) == BT_ESHAPE
+    assert bwd(segs(), ws=FAKE_MIS) == BT_EALIGN
+    # stored-dS scratch: B H Tq Tk floats when every position is a multiple of 128, else none
+    g = bt.cp_segments(256, [0, 512], [256, 768])
+    assert lib.bt_attention_block_bwd_ws_bytes(2, 3, 64, ctypes.byref(g)) == 2 * 3 * 512 * 512 * 4
+    g1 = bt.cp_segments(256, [0], [256, 768])
+    assert lib.bt_attention_block_bwd_ws_bytes(1, 1, 64, ctypes.byref(g1)) == 256 * 512 * 4
+    assert lib.bt_attention_block_bwd_ws_bytes(1, 1, 64, ctypes.byref(bt.cp_segments(256, [32], [0]))) == 0
+    assert lib.bt_attention_block_bwd_ws_bytes(1, 1, 64, None) == 0
     assert lib.bt_attention_lse_merge(FAKE, FAKE, FAKE, FAKE, 1, 16, 2, 6, None) == BT_ESHAPE
     assert lib.bt_attention_lse_merge(FAKE, FAKE, None, FAKE, 1, 16, 2, 8, None) == BT_EINVAL
     assert lib.bt_attention_rowdot(FAKE, FAKE, FAKE, 1, 16, 2, 132, None) == BT_ESHAPE

@@ -103,6 +103,91 @@ def test_block_fwd_single_segments_unaligned_to_tiles():
         _check_block(host(out).reshape(B, seg, H, hd), host(lse), r_out, r_lse, f"q{qp} k{kp}")
 
 
+@pytest.mark.parametrize("B,T,W,H,hd,pairs", [
+    (2, 1024, 2, 2, 64, [(0, 0), (0, 1), (1, 0)]),
+    (1, 2048, 4, 2, 32, [(0, 3), (3, 0), (2, 2)]),
+    (1, 1024, 2, 2, 128, [(1, 0), (1, 1)]),
+])
+@pytest.mark.parametrize("stored", [False, True])
+def test_block_bwd_vs_oracle(B, T, W, H, hd, pairs, stored):
+    """One ring step's backward with the step's own lse and D (the gradient of
+    that shard's attention alone), both methods; dQ, dK, dV added onto
+    nonzero accumulators."""
+    torch = torch_gpu()
+    C = H * hd
+    qkv = RNG.standard_normal((B, T, 3, H, hd)).astype(np.float32)
+    dout = RNG.standard_normal((B, T, H, hd)).astype(np.float32)
+    q, k, v = ops.split_qkv(qkv, H)
+    do = _heads(dout, H)
+    for r, s_ in pairs:
+        say(f"block bwd B={B} T={T} W={W} hd={hd} rank {r} shard {s_} stored={stored}")
+        pr, ps = cp.rank_positions(T, W, r), cp.rank_positions(T, W, s_)
+        Tl = len(pr)
+        qkv_r = dev(torch, _local(qkv, pr).reshape(B * Tl, 3 * C))
+        qkv_s = dev(torch, _local(qkv, ps).reshape(B * Tl, 3 * C))
+        do_r = dev(torch, _local(dout, pr).reshape(B * Tl, C))
+        segs = bt.bt_cp_rank_segments(T, W, r, s_)
+        out = torch.empty((B * Tl, C), device="cuda")
+        lse = torch.empty((B, H, Tl), device="cuda")
+        bt.bt_attention_block_fwd(qkv_r, qkv_s[:, C:], 3 * C, out, lse, 0, B, H, hd, segs)
+        D = torch.empty((B, H, Tl), device="cuda")
+        bt.bt_attention_rowdot(do_r, out, D, B, Tl, H, hd)
+        acc0 = RNG.standard_normal((B * Tl, 3 * C)).astype(np.float32)
+        dq = dev(torch, acc0)
+        dkv = dev(torch, acc0[:, ::-1])  # another nonzero start for dK/dV
+        need = bt.bt_attention_block_bwd_ws_bytes(B, H, hd, segs)
+        assert need == B * H * Tl * Tl * 4
+        ws = torch.empty(need, dtype=torch.uint8, device="cuda") if stored else None
+        bt.bt_attention_block_bwd(do_r, qkv_r, qkv_s[:, C:], 3 * C, lse, D, dq, dkv[:, C:], 3, B, H, hd, segs, ws=ws)
+        r_out, r_lse = cp.block_attention_fwd(q[:, :, pr], k[:, :, ps], v[:, :, ps], pr, ps)
+        r_D = (do[:, :, pr] * r_out).sum(axis=-1)
+        r_dq, r_dk, r_dv = cp.block_attention_bwd(do[:, :, pr], q[:, :, pr], k[:, :, ps], v[:, :, ps], pr, ps,
+                                                  r_lse, r_D)
+        g = host(dq).reshape(B, Tl, 3, H, hd)
+        gk = host(dkv).reshape(B, Tl, 3, H, hd)
+        a0 = acc0.reshape(B, Tl, 3, H, hd).astype(np.float64)
+        a1 = np.ascontiguousarray(acc0[:, ::-1]).reshape(B, Tl, 3, H, hd).astype(np.float64)
+        scale = max(np.abs(r_dq).max(), np.abs(r_dk).max(), np.abs(r_dv).max())
+        assert_close_maxabs(g[:, :, 0] - a0[:, :, 0], r_dq.transpose(0, 2, 1, 3), 1e-4, "dQ", scale=scale)
+        assert_close_maxabs(gk[:, :, 1] - a1[:, :, 1], r_dk.transpose(0, 2, 1, 3), 1e-4, "dK", scale=scale)
+        assert_close_maxabs(gk[:, :, 2] - a1[:, :, 2], r_dv.transpose(0, 2, 1, 3), 1e-4, "dV", scale=scale)
+        assert np.array_equal(g[:, :, 1:], a0[:, :, 1:])       # K, V parts of dqkv untouched
+        assert np.array_equal(gk[:, :, 0], a1[:, :, 0])         # Q part of the shard's buffer untouched
+
+
+def test_block_bwd_methods_agree():
+    """Same key-major pass in both methods: dK and dV bitwise equal; dQ
+    (stored dS times K on the matrix-core GEMM vs recomputation) to rounding."""
+    torch = torch_gpu()
+    B, T, W, H, hd = 2, 2048, 4, 3, 64
+    C = H * hd
+    qkv = RNG.standard_normal((B, T, 3, H, hd)).astype(np.float32)
+    dout = RNG.standard_normal((B, T, H, hd)).astype(np.float32)
+    for r, s_ in [(1, 1), (1, 3), (3, 1)]:
+        pr, ps = cp.rank_positions(T, W, r), cp.rank_positions(T, W, s_)
+        Tl = len(pr)
+        qkv_r = dev(torch, _local(qkv, pr).reshape(B * Tl, 3 * C))
+        qkv_s = dev(torch, _local(qkv, ps).reshape(B * Tl, 3 * C))
+        do_r = dev(torch, _local(dout, pr).reshape(B * Tl, C))
+        segs = bt.bt_cp_rank_segments(T, W, r, s_)
+        out = torch.empty((B * Tl, C), device="cuda")
+        lse = torch.empty((B, H, Tl), device="cuda")
+        bt.bt_attention_block_fwd(qkv_r, qkv_s[:, C:], 3 * C, out, lse, 0, B, H, hd, segs)
+        D = torch.empty((B, H, Tl), device="cuda")
+        bt.bt_attention_rowdot(do_r, out, D, B, Tl, H, hd)
+        res = []
+        for ws in (None, torch.empty(bt.bt_attention_block_bwd_ws_bytes(B, H, hd, segs), dtype=torch.uint8,
+                                     device="cuda")):
+            dq = torch.zeros((B * Tl, 3 * C), device="cuda")
+            dkv = torch.zeros((B * Tl, 3 * C), device="cuda")
+            bt.bt_attention_block_bwd(do_r, qkv_r, qkv_s[:, C:], 3 * C, lse, D, dq, dkv[:, C:], 0, B, H, hd, segs,
+                                      ws=ws)
+            res.append((host(dq), host(dkv)))
+        (q0, k0), (q1, k1) = res
+        assert np.array_equal(k0, k1), f"r{r} s{s_}: dK/dV differ between methods"
+        assert_close_maxabs(q1, q0, 1e-5, f"r{r} s{s_}: dQ stored vs recomputed", scale=max(np.abs(q0).max(), 1e-30))
+
+
 def test_fused_merge_vs_oracle():
     """merge = 1 folds the shard into a running state, including rows whose
     state is empty (they take the block) and rows whose block is empty (they
@@ -162,9 +247,9 @@ def test_lse_merge_standalone_vs_oracle():
     assert_close_maxabs(g_o, r_o.transpose(0, 2, 1, 3), 1e-5, "out")
 
 
-def _gpu_ring(torch, qkv, dout, T, W, H, hd, packed_grad=False):
+def _gpu_ring(torch, qkv, dout, T, W, H, hd, stored=True):
     """All ranks on one GPU through the ring schedule; returns global-order
-    (out, lse, dqkv)."""
+    (out, lse, dqkv).  stored: the stored-dS backward (else recompute)."""
     B = qkv.shape[0]
     C = H * hd
     pos = [cp.rank_positions(T, W, r) for r in range(W)]
@@ -175,8 +260,11 @@ def _gpu_ring(torch, qkv, dout, T, W, H, hd, packed_grad=False):
     do_l = [dev(torch, _local(dout, p).reshape(B * Tl, C)) for p in pos] if dout is not None else None
     D = [torch.empty((B, H, Tl), device="cuda") for _ in range(W)]
     dq = [torch.full((B * Tl, 3 * C), float("nan"), device="cuda") for _ in range(W)]
+    ws = None
+    if stored:
+        ws = torch.empty(ring.ws_bytes(W, T, B, H, hd), dtype=torch.uint8, device="cuda")
     ring.emulate(W, T, B, H, hd, qkv_l, out, lse, lambda s: (qkv_l[s][:, C:], 3 * C),
-                 dout=do_l, D=D, dqkv=dq, dkv_of=lambda s: dq[s][:, C:])
+                 dout=do_l, D=D, dqkv=dq, dkv_of=lambda s: dq[s][:, C:], ws=ws)
     g_out = np.empty((B, T, H, hd))
     g_lse = np.empty((B, H, T))
     g_d = np.empty((B, T, 3, H, hd))
@@ -189,12 +277,13 @@ def _gpu_ring(torch, qkv, dout, T, W, H, hd, packed_grad=False):
 
 
 @pytest.mark.parametrize("B,T,W,H,hd", [(1, 1024, 2, 2, 64), (2, 2048, 4, 2, 64), (1, 768, 3, 2, 128)])
-def test_ring_emulation_vs_oracle(B, T, W, H, hd):
+@pytest.mark.parametrize("stored", [False, True])
+def test_ring_emulation_vs_oracle(B, T, W, H, hd, stored):
     torch = torch_gpu()
     qkv = RNG.standard_normal((B, T, 3, H, hd)).astype(np.float32)
     dout = RNG.standard_normal((B, T, H, hd)).astype(np.float32)
-    say(f"ring emulation B={B} T={T} W={W} H={H} hd={hd}")
-    g_out, g_lse, g_d = _gpu_ring(torch, qkv, dout, T, W, H, hd)
+    say(f"ring emulation B={B} T={T} W={W} H={H} hd={hd} stored={stored}")
+    g_out, g_lse, g_d = _gpu_ring(torch, qkv, dout, T, W, H, hd, stored)
     say("oracle ring")
     r_out, r_lse = cp.ring_attention_fwd(qkv, H, W)
     r_d = cp.ring_attention_bwd(dout, qkv, H, W)

@@ -23,12 +23,12 @@ def test_emulate_issues_the_ring_in_order(monkeypatch):
     monkeypatch.setattr(bt, "bt_attention_rowdot",
                         lambda dout, out, D, B, T, H, hd, stream: calls.append(("D", dout, out, D, T)))
     monkeypatch.setattr(bt, "bt_attention_block_bwd",
-                        lambda dout, qkv, kv, ks, lse, D, dqkv, dkv, acc, B, H, hd, segs, stream:
-                        calls.append(("bwd", segs[1], segs[2], acc, dqkv, dkv)))
+                        lambda dout, qkv, kv, ks, lse, D, dqkv, dkv, acc, B, H, hd, segs, ws=None, stream=None:
+                        calls.append(("bwd", segs[1], segs[2], acc, dqkv, dkv, ws)))
     W, T = 4, 4096
     names = lambda p: [f"{p}{r}" for r in range(W)]
     ring.emulate(W, T, 2, 12, 64, names("qkv"), names("out"), names("lse"), lambda s: (f"kv{s}", 2304),
-                 dout=names("do"), D=names("D"), dqkv=names("dqkv"), dkv_of=lambda s: f"dkv{s}")
+                 dout=names("do"), D=names("D"), dqkv=names("dqkv"), dkv_of=lambda s: f"dkv{s}", ws="scratch")
     fwd = [c for c in calls if c[0] == "fwd"]
     bwd = [c for c in calls if c[0] == "bwd"]
     assert len(fwd) == W * W and len(bwd) == W * W
@@ -42,7 +42,7 @@ def test_emulate_issues_the_ring_in_order(monkeypatch):
     for k, c in enumerate(bwd):
         i, r = divmod(k, W)
         s = (r - i) % W
-        assert c[1:] == (r, s, 3 if i else 0, f"dqkv{r}", f"dkv{s}")
+        assert c[1:] == (r, s, 3 if i else 0, f"dqkv{r}", f"dkv{s}", "scratch")
     # every shard gradient is written once (its owner, step 0) before it is added to
     first = {}
     for c in bwd:
