@@ -275,17 +275,21 @@ def test_embedding_brute_force():
 
 # ---------------------------------------------------------------------- AdamW
 def test_adamw_closed_form_t1():
+    rng = np.random.default_rng(277)  # own stream: independent of test order
     n = 64
-    p0 = RNG.standard_normal(n)
-    g = RNG.standard_normal(n) * 1e-2
+    p0 = rng.standard_normal(n)
+    g = rng.standard_normal(n) * 1e-2
     g[3] = 0.0
     lr, wd, eps = 3e-4, 0.1, 1e-8
     mask = (np.arange(n) < 40).astype(float)
     p1, m1, v1 = ops.adamw(p0, g, np.zeros(n), np.zeros(n), 1, lr, 0.9, 0.999, eps, wd, mask)
     expect = p0 - lr * (wd * p0 * mask + g / (np.abs(g) + eps))
-    assert np.allclose(p1, expect, rtol=0, atol=1e-15)
-    # g = 0: only decay acts
-    assert abs(p1[3] - p0[3] * (1 - lr * wd)) < 1e-16
+    # the closed form and the oracle's update order round differently: a few
+    # ulps of the parameter
+    ulp = np.finfo(np.float64).eps
+    assert np.all(np.abs(p1 - expect) <= 4 * ulp * np.maximum(np.abs(p0), 1.0))
+    # g = 0: only decay acts (p0 - lr wd p0 and p0 (1 - lr wd) differ only in rounding)
+    assert abs(p1[3] - p0[3] * (1 - lr * wd)) <= 4 * ulp * abs(p0[3])
     # clip coefficient c scales g before the moments; at t=1 the update is
     # sign-like so only m and v see it
     _, mc, vc = ops.adamw(p0, g, np.zeros(n), np.zeros(n), 1, lr, 0.9, 0.999, eps, wd, mask, 0.25)
