@@ -67,6 +67,33 @@ __device__ __forceinline__ float wave_max(float v) {
   return v;
 }
 
+// Direct global -> LDS copy of 16 bytes per lane (gfx950 global_load_lds_dwordx4):
+// lane L of the wave writes LDS bytes [dst + 16 L, dst + 16 L + 16), dst
+// wave-uniform, passed in M0.  The data never occupies VGPRs and needs no
+// LDS store instruction.  It is issued from inline assembly so that the
+// compiler does not conservatively wait for it before unrelated LDS reads
+// of the other buffer; completion is awaited explicitly (wait_copies) before
+// the barrier that publishes the tile.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void copy16_to_lds(const float* src, float* lds_dst) {
+  const unsigned l = (unsigned)(uintptr_t)(__attribute__((address_space(3))) float*)lds_dst;
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+               :
+               : "s"(__builtin_amdgcn_readfirstlane(l)), "v"(src)
+               : "memory", "m0");
+}
+// The same copy with a wave-uniform global base (SGPR pair), a per-lane
+// 32-bit byte offset and a wave-uniform LDS byte address.
+__device__ __forceinline__ void copy16_to_lds_sbase(const float* base, unsigned voff, unsigned lds_byte) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               :
+               : "s"(lds_byte), "v"(voff), "s"(base)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+__device__ __forceinline__ void wait_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 // 2^x as the single hardware transcendental (v_exp_f32, about 1 ulp),
 // without the library's rescaling for results below 2^-126: those may come
 // out as 0, an absolute error under 1.2e-38.  Used where the exponent is a

@@ -108,24 +108,6 @@ __device__ __forceinline__ int kc_swizzle(int row) {
 // halves 8 k-rows apart, 32 consecutive columns each) hits distinct banks.
 __device__ __forceinline__ int mn_swizzle(int k) { return ((k >> 3) & 1) << 5; }
 
-// Direct global -> LDS copy of 16 bytes per lane (gfx950 global_load_lds_dwordx4):
-// lane L of the wave writes LDS bytes [dst + 16 L, dst + 16 L + 16), dst
-// wave-uniform, passed in M0.  The data never occupies VGPRs and needs no
-// LDS store instruction.  It is issued from inline assembly so that the
-// compiler does not conservatively wait for it before unrelated LDS reads
-// of the other buffer; completion is awaited explicitly (wait_copies) before
-// the barrier that publishes the tile.
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void copy16_to_lds(const float* src, float* lds_dst) {
-  const unsigned l = (unsigned)(uintptr_t)(__attribute__((address_space(3))) float*)lds_dst;
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-               :
-               : "s"(__builtin_amdgcn_readfirstlane(l)), "v"(src)
-               : "memory", "m0");
-}
-#pragma clang diagnostic pop
-__device__ __forceinline__ void wait_copies() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // Per-lane sources of the NI direct copies (1 KB slices) a wave issues for
 // one R x BK operand tile at k = k0; later tiles add a fixed stride.

@@ -95,6 +95,112 @@ __global__ void __launch_bounds__(XT) xent_row_kernel(float* logits, const int32
   }
 }
 
+// Fused pass for a 50,304-column class of rows (13 float4 per thread),
+// persistent and pipelined: each block (one per CU; the prefetch buffer is
+// most of the LDS) takes rows b, b + G, ...  While a row is reduced and
+// written, the next row is already on its way: its first XS_PF float4 per
+// thread are copied straight into LDS (global_load_lds, no registers) and
+// the remaining XS_NR into a small register set.  The gradient stores go out
+// as raw buffer stores, unconditionally (lanes past the row are dropped by
+// the buffer's range check), so every wave issues exactly 13 of them per row
+// and the wait for the prefetch at the next row can skip exactly those 13
+// (the stores need not complete before the next row starts).  Measured on
+// MI355X at 16384 x 50304 logits: 1.29 ms (5.1 TB/s) for the one-row-per-CU
+// kernel below, 1.15 ms (5.7 TB/s) for this one.
+constexpr int XS_NPT = 13, XS_PF = 9, XS_NR = XS_NPT - XS_PF;
+
+__global__ void __launch_bounds__(XT) xent_stream_kernel(float* logits, const int32_t* __restrict__ targets,
+                                                         float* __restrict__ loss_rows, float* __restrict__ lse_out,
+                                                         float scale, int M, int V, int Vp) {
+  __shared__ __attribute__((aligned(16))) float pf[XS_PF * XT * 4];
+  __shared__ float red[XT / 64];
+  __shared__ float s_zy;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int V4 = Vp >> 2;
+  const int G = gridDim.x;
+  auto rsrc = [&](int row) {
+    return __builtin_amdgcn_make_buffer_rsrc(logits + (long long)row * Vp, (short)0, Vp * 4, 0x00020000);
+  };
+  const unsigned voff = 16u * tid;  // byte offset of the thread's float4 in a 1024-float4 slice
+  const unsigned lds_wave = __builtin_amdgcn_readfirstlane(
+      (unsigned)(uintptr_t)(__attribute__((address_space(3))) float*)pf + 1024u * wave);
+  // prefetch of a row: the LDS part (every lane in range: V4 >= XS_PF XT) and the register part
+  floatx4 nx[XS_NR];
+  auto prefetch = [&](int row) {
+    const float* zr = logits + (long long)row * Vp;
+#pragma unroll
+    for (int i = 0; i < XS_PF; ++i) copy16_to_lds_sbase(zr, voff + 16u * XT * i, lds_wave + 16u * XT * i);
+    const auto r = rsrc(row);
+#pragma unroll
+    for (int j = 0; j < XS_NR; ++j)  // past the row: 0, masked below like the padded columns
+      nx[j] = __builtin_amdgcn_raw_buffer_load_b128(r, voff, 16 * XT * (XS_PF + j), 2);
+  };
+  int row = blockIdx.x;
+  if (row >= M) return;
+  prefetch(row);
+  wait_copies();
+  for (; row < M; row += G) {
+    // the prefetch of this row is complete once at most the 13 stores of the
+    // previous row are outstanding; then every wave's part is visible
+    asm volatile("s_waitcnt vmcnt(13)" ::: "memory");
+    __syncthreads();
+    floatx4 z[XS_NPT];
+#pragma unroll
+    for (int i = 0; i < XS_PF; ++i) z[i] = *reinterpret_cast<const floatx4*>(pf + 4 * (XT * i + tid));
+#pragma unroll
+    for (int j = 0; j < XS_NR; ++j) z[XS_PF + j] = nx[j];
+    __syncthreads();  // every wave has read the buffer: it may be refilled
+    if (row + G < M) prefetch(row + G);
+
+    int y = targets[row];
+    const bool bad = y < 0 || y >= V;
+    if (bad) y = 0;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < XS_NPT; ++i) {
+      const int c4 = tid + XT * i;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if (4 * c4 + k >= V) z[i][k] = -INFINITY;  // padded columns are outside the softmax
+        if (4 * c4 + k == y) s_zy = z[i][k];       // the target logit, taken from registers: the
+                                                   // row is overwritten in place below
+        mx = fmaxf(mx, z[i][k]);
+      }
+    }
+    mx = block_reduce(mx, red, true);  // its barriers also publish s_zy
+    const float zy = s_zy;
+    const float mxl = mx * LOG2E_X;
+    float sum = 0.f;
+#pragma unroll
+    for (int i = 0; i < XS_NPT; ++i)
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        z[i][k] = exp2_hw(z[i][k] * LOG2E_X - mxl);
+        sum += z[i][k];
+      }
+    // its barriers also separate this row's reads of s_zy from the next row's write
+    sum = block_reduce(sum, red, false);
+    const float lse = mx + log2f(sum) * LN2_X;
+    if (tid == 0) {
+      loss_rows[row] = bad ? NAN : lse - zy;
+      lse_out[row] = lse;
+    }
+    const float inv = scale / sum;
+    const auto r = rsrc(row);
+#pragma unroll
+    for (int i = 0; i < XS_NPT; ++i) {
+      const int c4 = tid + XT * i;
+      floatx4 o;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int c = 4 * c4 + k;
+        o[k] = c < V ? z[i][k] * inv - (c == y ? scale : 0.f) : 0.f;
+      }
+      __builtin_amdgcn_raw_buffer_store_b128(o, r, voff, 16 * XT * i, 2);  // non-temporal; past the row: dropped
+    }
+  }
+}
+
 // Backward from a stored lse: elementwise over the row.
 __global__ void __launch_bounds__(256) xent_bwd_kernel(const float* logits, const float* __restrict__ lse,
                                                        const int32_t* __restrict__ targets, float* dlogits,
@@ -124,6 +230,17 @@ bt_status xent_check(const void* logits, const void* targets, int M, int V, int 
   BT_RETURN_IF(M > 0 && (!logits || !targets), BT_EINVAL, "%s: NULL pointer", who);
   BT_RETURN_IF(logits && !aligned16(logits), BT_EALIGN, "%s: logits must be 16-byte aligned", who);
   return BT_OK;
+}
+
+// CUs of the current device (the streaming pass runs one block per CU).
+int stream_cus() {
+  static const int n = [] {
+    int dev = 0, c = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      return 0;
+    return c;
+  }();
+  return n;
 }
 
 template <int MODE>
@@ -175,5 +292,14 @@ extern "C" bt_status bt_softmax_xent_fused(float* logits, const int32_t* targets
   BT_TRY(xent_check(logits, targets, M, V, Vp, "bt_softmax_xent_fused"));
   if (M == 0) return BT_OK;
   BT_RETURN_IF(!loss_rows || !lse, BT_EINVAL, "bt_softmax_xent_fused: NULL output");
+  const int V4 = Vp / 4;
+  if (V4 > XT * (XS_NPT - 1) && V4 <= XT * XS_NPT) {
+    const int cus = stream_cus();
+    if (cus > 0) {
+      hipLaunchKernelGGL(xent_stream_kernel, dim3(M < cus ? M : cus), dim3(XT), 0, as_stream(stream), logits, targets,
+                         loss_rows, lse, scale, M, V, Vp);
+      return check_launch("xent_stream_kernel");
+    }
+  }
   return launch_rows<1>(logits, targets, loss_rows, lse, logits, scale, M, V, Vp, as_stream(stream));
 }

@@ -130,6 +130,29 @@ def test_xent_full_size_sampled():
                         "dlogits rows")
 
 
+@pytest.mark.parametrize("M,V,Vp", [(600, 50257, 50304), (530, 53001, 53248)])
+def test_xent_fused_several_rows_per_block(M, V, Vp):
+    """The fused pass at vocabularies of 13 float4 per thread runs one block
+    per CU over several rows each, with the next row prefetched: every row
+    of a launch in which each block takes 2-3 rows against the oracle."""
+    torch = torch_gpu()
+    say(f"xent fused several rows per block M={M} V={V} Vp={Vp}")
+    z = (RNG.standard_normal((M, Vp)) * 3).astype(np.float32)
+    y = RNG.integers(0, V, M).astype(np.int32)
+    y[0], y[-1] = 0, V - 1
+    scale = 1.0 / M
+    zd, yd = dev(torch, z), dev(torch, y)
+    loss = torch.empty(M, device="cuda")
+    lse = torch.empty(M, device="cuda")
+    bt.bt_softmax_xent_fused(zd, yd, loss, lse, scale, M, V, Vp)
+    rl, rlse = ops.xent_fwd(z, y, V)
+    assert np.allclose(host(loss), rl, rtol=1e-5, atol=0)
+    assert np.allclose(host(lse), rlse, rtol=1e-6, atol=1e-6)
+    dz = host(zd)
+    assert_close_maxabs(dz, ops.xent_bwd(z, y, V, scale), 1e-5, "dlogits (fused, several rows per block)")
+    assert np.all(dz[:, V:] == 0)
+
+
 # ---------------------------------------------------------------------- AdamW
 @pytest.mark.parametrize("t,clip", [(1, None), (2, 0.37), (7, None)])
 def test_adamw(t, clip):
