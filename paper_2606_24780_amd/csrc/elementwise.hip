@@ -146,15 +146,23 @@ __global__ void __launch_bounds__(EW_THREADS) sumsq_kernel(const floatx4* __rest
   }
 }
 
-// Stage 2: one block; fixed-order sum of partials, then norm and clip coef.
-__global__ void __launch_bounds__(EW_THREADS) norm_finish_kernel(const double* __restrict__ part, int nparts,
-                                                                 float clip, float* out_norm, float* out_coef) {
-  __shared__ double red[EW_THREADS];
+// Stage 2: one block of NF threads; fixed-order sum of partials (each
+// thread a strided set, loads unrolled so several are in flight), then the
+// norm and the clip coefficient.
+constexpr int NF = 1024;
+__global__ void __launch_bounds__(NF) norm_finish_kernel(const double* __restrict__ part, int nparts, float clip,
+                                                         float* out_norm, float* out_coef) {
+  __shared__ double red[NF];
   double s = 0.0;
-  for (int i = threadIdx.x; i < nparts; i += blockDim.x) s += part[i];
+  int i = threadIdx.x;
+  for (; i + 3 * NF < nparts; i += 4 * NF) {
+    const double a = part[i], b = part[i + NF], c = part[i + 2 * NF], d = part[i + 3 * NF];
+    s += ((a + b) + (c + d));
+  }
+  for (; i < nparts; i += NF) s += part[i];
   red[threadIdx.x] = s;
   __syncthreads();
-  for (int w = EW_THREADS / 2; w >= 1; w >>= 1) {
+  for (int w = NF / 2; w >= 1; w >>= 1) {
     if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
     __syncthreads();
   }
@@ -349,7 +357,7 @@ extern "C" bt_status bt_grad_norm_clip(const float* g, size_t n, float clip, flo
   double* part = static_cast<double*>(ws);
   hipLaunchKernelGGL(sumsq_kernel, dim3(nb), dim3(EW_THREADS), 0, s, reinterpret_cast<const floatx4*>(g), n4, part);
   BT_TRY(check_launch("sumsq_kernel"));
-  hipLaunchKernelGGL(norm_finish_kernel, dim3(1), dim3(EW_THREADS), 0, s, part, (int)nb, clip, out_norm, out_coef);
+  hipLaunchKernelGGL(norm_finish_kernel, dim3(1), dim3(NF), 0, s, part, (int)nb, clip, out_norm, out_coef);
   return check_launch("norm_finish_kernel");
 }
 
