@@ -15,57 +15,68 @@ namespace {
 
 constexpr int ROWS_PER_BLOCK = 4;  // 4 waves
 
-template <int NV>
+// RPW rows per wave (consecutive), all rows' loads issued before any row is
+// reduced, so a wave keeps RPW rows of x in flight.
+template <int NV, int RPW>
 __global__ void __launch_bounds__(256) ln_fwd_kernel(const float* __restrict__ x,
                                                      const float* __restrict__ gamma,
                                                      const float* __restrict__ beta,
                                                      float* __restrict__ y, float* __restrict__ mean,
                                                      float* __restrict__ rstd, int M, int C, float eps) {
   const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * ROWS_PER_BLOCK + (threadIdx.x >> 6);
-  if (row >= M) return;
+  const int row0 = (blockIdx.x * ROWS_PER_BLOCK + (threadIdx.x >> 6)) * RPW;
+  if (row0 >= M) return;
   const int C4 = C >> 2;
-  const floatx4* xr = reinterpret_cast<const floatx4*>(x + (long long)row * C);
-  floatx4 v[NV];
-  float s = 0.f;
+  floatx4 v[RPW][NV];
 #pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    const int c = lane + 64 * i;
-    v[i] = c < C4 ? xr[c] : floatx4{0.f, 0.f, 0.f, 0.f};
-    s += (v[i][0] + v[i][1]) + (v[i][2] + v[i][3]);
-  }
-  const float mu = wave_sum(s) / (float)C;
-  float q = 0.f;
+  for (int r = 0; r < RPW; ++r) {
+    const floatx4* xr = reinterpret_cast<const floatx4*>(x + (long long)(row0 + r) * C);
 #pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    const int c = lane + 64 * i;
-    if (c < C4) {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        const float d = v[i][k] - mu;
-        q += d * d;
-      }
+    for (int i = 0; i < NV; ++i) {
+      const int c = lane + 64 * i;
+      v[r][i] = (c < C4 && row0 + r < M) ? xr[c] : floatx4{0.f, 0.f, 0.f, 0.f};
     }
   }
-  const float var = wave_sum(q) / (float)C;
-  const float rs = 1.0f / sqrtf(var + eps);
-  floatx4* yr = reinterpret_cast<floatx4*>(y + (long long)row * C);
   const floatx4* g4 = reinterpret_cast<const floatx4*>(gamma);
   const floatx4* b4 = reinterpret_cast<const floatx4*>(beta);
 #pragma unroll
-  for (int i = 0; i < NV; ++i) {
-    const int c = lane + 64 * i;
-    if (c < C4) {
-      const floatx4 g = g4[c], b = b4[c];
-      floatx4 o;
+  for (int r = 0; r < RPW; ++r) {
+    const int row = row0 + r;
+    if (row >= M) break;
+    float s = 0.f;
 #pragma unroll
-      for (int k = 0; k < 4; ++k) o[k] = (v[i][k] - mu) * rs * g[k] + b[k];
-      yr[c] = o;
+    for (int i = 0; i < NV; ++i) s += (v[r][i][0] + v[r][i][1]) + (v[r][i][2] + v[r][i][3]);
+    const float mu = wave_sum(s) / (float)C;
+    float q = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c = lane + 64 * i;
+      if (c < C4) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          const float d = v[r][i][k] - mu;
+          q += d * d;
+        }
+      }
     }
-  }
-  if (lane == 0) {
-    mean[row] = mu;
-    rstd[row] = rs;
+    const float var = wave_sum(q) / (float)C;
+    const float rs = 1.0f / sqrtf(var + eps);
+    floatx4* yr = reinterpret_cast<floatx4*>(y + (long long)row * C);
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c = lane + 64 * i;
+      if (c < C4) {
+        const floatx4 g = g4[c], b = b4[c];
+        floatx4 o;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) o[k] = (v[r][i][k] - mu) * rs * g[k] + b[k];
+        yr[c] = o;
+      }
+    }
+    if (lane == 0) {
+      mean[row] = mu;
+      rstd[row] = rs;
+    }
   }
 }
 
@@ -100,7 +111,7 @@ __device__ __forceinline__ void ln_row_load(LnRow<NV>& r, const float* dy, const
   for (int i = 0; i < NV; ++i) {
     const int c = lane + 64 * i;
     r.d[i] = c < C4 ? dyr[c] : floatx4{0.f, 0.f, 0.f, 0.f};
-    xv[i] = c < C4 ? xr[c] : floatx4{0.f, 0.f, 0.f, 0.f};
+    xv[i] = c < C4 ? __builtin_nontemporal_load(xr + c) : floatx4{0.f, 0.f, 0.f, 0.f};  // x: read once here
     r.old[i] = (accumulate && c < C4) ? dxr[c] : floatx4{0.f, 0.f, 0.f, 0.f};
   }
   float s1 = 0.f, s2 = 0.f;
@@ -264,9 +275,11 @@ extern "C" bt_status bt_layernorm_fwd(const float* x, const float* gamma, const 
                "bt_layernorm_fwd: x, y, gamma, beta must be 16-byte aligned");
   BT_RETURN_IF(x == y, BT_EINVAL, "bt_layernorm_fwd: y must not alias x");
   BT_RETURN_IF(!(eps >= 0.f), BT_EINVAL, "bt_layernorm_fwd: eps must be >= 0");
-  dim3 grid((M + ROWS_PER_BLOCK - 1) / ROWS_PER_BLOCK);
+  // two rows per wave where the row fits 4 float4 per lane (C <= 1024)
+  const int rpw = ln_nv(C) <= 4 ? 2 : 1;
+  dim3 grid((M + ROWS_PER_BLOCK * rpw - 1) / (ROWS_PER_BLOCK * rpw));
   hipStream_t s = as_stream(stream);
-#define BT_LN_FWD(NV) hipLaunchKernelGGL(ln_fwd_kernel<NV>, grid, dim3(256), 0, s, x, gamma, beta, y, mean, rstd, M, C, eps)
+#define BT_LN_FWD(NV) hipLaunchKernelGGL((ln_fwd_kernel<NV, (NV <= 4 ? 2 : 1)>), grid, dim3(256), 0, s, x, gamma, beta, y, mean, rstd, M, C, eps)
   BT_LN_DISPATCH(ln_nv(C), BT_LN_FWD)
 #undef BT_LN_FWD
   return check_launch("ln_fwd_kernel");
