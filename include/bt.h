@@ -86,7 +86,9 @@ typedef enum {
  * dW = X^T dY, computed from the dY tiles the product already reads.  It
  * requires opB = BT_OP_N, epi = BT_EPI_NONE and no residual.
  * ws may be NULL when bt_gemm_ws_bytes() returns 0 for the shape; otherwise
- * it must hold that many bytes (split-K partial products).
+ * it must hold that many bytes (split-K partial products; any epilogue may
+ * be split, which applies it in the fixed-order reduction of the partials).
+ * Too small a workspace for a split shape: BT_EWORKSPACE, nothing launched.
  */
 bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K,
                   const float* A, int lda, const float* B, int ldb,

@@ -331,7 +331,12 @@ extern "C" bt_status bt_adamw_step(float* p, const float* g, float* m, float* v,
   a.inv_bc1 = (float)(1.0 / (1.0 - pow(beta1, (double)t)));
   a.inv_bc2 = (float)(1.0 / (1.0 - pow(beta2, (double)t)));
   const size_t n4 = n / 4;
-  hipLaunchKernelGGL(adamw_kernel, dim3(ew_blocks(n4)), dim3(EW_THREADS), 0, as_stream(stream),
+  // one group of STREAM_U float4 per thread: a grid-stride loop would make each
+  // group's loads wait behind the previous group's stores (one VMEM counter)
+  size_t nb = (n4 + (size_t)EW_THREADS * STREAM_U - 1) / ((size_t)EW_THREADS * STREAM_U);
+  if (nb > (1u << 30)) nb = 1u << 30;
+  if (nb < 1) nb = 1;
+  hipLaunchKernelGGL(adamw_kernel, dim3((unsigned)nb), dim3(EW_THREADS), 0, as_stream(stream),
                      reinterpret_cast<floatx4*>(p), reinterpret_cast<const floatx4*>(g),
                      reinterpret_cast<floatx4*>(m), reinterpret_cast<floatx4*>(v), n4, n_decay / 4, a,
                      grad_scale);

@@ -505,10 +505,14 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
     }
 }
 
-// Fixed-order sum of split-K partials: C = sum_z ws[z] + beta * C.
-__global__ void __launch_bounds__(256) splitk_reduce(const float* __restrict__ ws, float* __restrict__ C,
-                                                     long long ldc, int M, int N, int splits,
-                                                     float beta) {
+// Fixed-order sum of split-K partials, then the product's epilogue, element
+// by element in the tile epilogue's order: v = sum_z ws[z]; bias (+ GELU,
+// storing the pre-activation) or the GELU-backward factor; + residual +
+// beta * C.
+template <int EPI>
+__global__ void __launch_bounds__(256) splitk_reduce(const GemmParams p) {
+  const float* __restrict__ ws = p.ws;
+  const int M = p.M, N = p.N, splits = p.splits;
   const long long n4 = (long long)M * (N / 4);
   const long long MN = (long long)M * N;
   for (long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x; e < n4;
@@ -516,11 +520,33 @@ __global__ void __launch_bounds__(256) splitk_reduce(const float* __restrict__ w
     const int i = (int)(e / (N / 4));
     const int j = (int)(e - (long long)i * (N / 4)) * 4;
     const float* w = ws + (long long)i * N + j;
-    floatx4 s = *reinterpret_cast<const floatx4*>(w);
-    for (int z = 1; z < splits; ++z) s += *reinterpret_cast<const floatx4*>(w + z * MN);
-    floatx4* c = reinterpret_cast<floatx4*>(C + (long long)i * ldc + j);
-    if (beta != 0.f) s += *c;
-    *c = s;
+    floatx4 v = *reinterpret_cast<const floatx4*>(w);
+    for (int z = 1; z < splits; ++z) v += *reinterpret_cast<const floatx4*>(w + z * MN);
+    const long long off = (long long)i * p.ldc + j;
+    // bias, pre-activation, GELU input and residual carry no alignment
+    // requirement beyond 4 bytes: element accesses
+    if (EPI == BT_EPI_BIAS || EPI == BT_EPI_BIAS_GELU) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) v[k] += p.bias[j + k];
+      if (EPI == BT_EPI_BIAS_GELU) {
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          if (p.preact) p.preact[off + k] = v[k];
+          v[k] = gelu_f(v[k]);
+        }
+      }
+    } else if (EPI == BT_EPI_DGELU) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) v[k] *= gelu_grad_f(p.gelu_in[off + k]);
+    }
+    floatx4* c = reinterpret_cast<floatx4*>(p.C + off);
+    floatx4 add = floatx4{0.f, 0.f, 0.f, 0.f};
+    if (p.residual) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) add[k] = p.residual[off + k];
+    }
+    if (p.beta != 0.f) add += *c;
+    *c = v + add;
   }
 }
 
@@ -536,21 +562,31 @@ __global__ void __launch_bounds__(256) splitk_colsum_reduce(const float* __restr
 }
 
 // Block-tile configurations: tile depth, wave grid (64 x 64 outputs per
-// wave), resident blocks per CU (= waves per SIMD for 4-wave blocks), and
-// the relative rate of one CU working
-// through 128 x 128 x 16 tile steps when it holds its full complement of
-// blocks (K-contiguous operand present / both operands MN-contiguous),
-// measured on MI355X.  Larger block tiles (256 x 128, 128 x 256, 256 x 256
-// with 64 x 64 per wave) and larger wave tiles (64 x 128 or 128 x 64 at 2
-// waves per SIMD; 128 x 128 spills) were measured slower on most of the
-// model's shapes and are not offered.
+// wave), 32 x 32 blocks per wave, resident blocks per CU (= waves per SIMD
+// for 4-wave blocks), and the launch model's constants, fitted on MI355X to
+// the measured time of every (tile, split) choice of the products of three
+// GPT-2 training steps (124M at 16384 tokens, 124M at 32768, 2.42B at 2048;
+// 1100 timings, 3.8% rms error; a fit without any one of the three picks
+// within 0.5% of the best measured choice on it):
+//  rate_kc / rate_mn  relative k-loop rate with a K-contiguous operand /
+//                     with both operands MN-contiguous;
+//  ovh                a block's cost outside the k-loop (pipeline fill,
+//                     epilogue, and the partial tile's round trip through
+//                     the workspace when split), in 128 x 128 x 16 steps;
+//  part[q]            rate of a last round in which a CU holds (q+1)/4 of
+//                     its full complement of blocks.
+// Larger block tiles (256 x 128, 128 x 256, 256 x 256 with 64 x 64 per
+// wave) and larger wave tiles (64 x 128 or 128 x 64 at 2 waves per SIMD;
+// 128 x 128 spills) were measured slower on most of the model's shapes and
+// are not offered.
 struct TileCfg {
   int bk, wm, wn, mb, nb, occ;
-  double rate_kc, rate_mn;
+  double rate_kc, rate_mn, ovh;
+  double part[3];
 };
 constexpr TileCfg kTileCfgs[] = {
-    {32, 2, 2, 2, 2, 2, 1.00, 1.00},
-    {16, 2, 2, 2, 2, 4, 1.0 / 0.95, 1.0 / 0.98},
+    {32, 2, 2, 2, 2, 2, 1.031, 1.013, 6.11, {0.90, 0.90, 0.90}},
+    {16, 2, 2, 2, 2, 4, 1.046, 1.038, 5.76, {0.88, 0.974, 0.987}},
 };
 constexpr int NUM_TILE_CFGS = (int)(sizeof(kTileCfgs) / sizeof(kTileCfgs[0]));
 
@@ -559,20 +595,24 @@ struct GemmCfg {
   int splits, ksplit;
 };
 
-// Relative time of a launch of `blocks` equal blocks (each `work` long): the
-// busiest CU holds ceil(blocks / NUM_CU) of them and runs up to `occ` at
-// once.  A last round with only one wave per SIMD resident keeps the matrix
-// pipe only partly busy (taken as 60%).
-double launch_time(long long blocks, int occ, int waves_per_block, double work) {
+// Relative time of a launch of `blocks` equal blocks (each `work` long) on
+// tile configuration c: the busiest CU holds ceil(blocks / NUM_CU) of them
+// and runs up to `occ` at once; a last, partial round runs at c.part[].
+double launch_time(const TileCfg& c, long long blocks, double work) {
+  const int occ = c.occ * 4 / (c.wm * c.wn);
   const long long per_cu = (blocks + NUM_CU - 1) / NUM_CU;
   const long long full = per_cu / occ, rem = per_cu % occ;
   double t = (double)(full * occ) * work;
-  if (rem) t += (double)rem * work / (rem * waves_per_block >= 8 ? 1.0 : 0.6);
+  if (rem) {
+    int q = (int)((4 * rem + occ / 2) / occ) - 1;
+    q = q < 0 ? 0 : q > 2 ? 2 : q;
+    t += (double)rem * work / c.part[q];
+  }
   return t;
 }
 
-// Tile configuration and K split for a shape.  Split-K (only for products
-// without an epilogue) adds a partial-tile round trip through the workspace.
+// Tile configuration and K split for a shape (a split product's epilogue
+// runs in the reduction of the partials).
 GemmCfg choose_config(int M, int N, int K, bool akc, bool bkc, bool may_split) {
   if (K <= 0) return GemmCfg{0, 1, 32};
   // Very long k-loops over K-contiguous rows of A with at least two tiles
@@ -582,7 +622,9 @@ GemmCfg choose_config(int M, int N, int K, bool akc, bool bkc, bool may_split) {
   const bool deep_only = K >= 32768 && akc && (long long)((M + 127) / 128) * ((N + 127) / 128) >= 2 * NUM_CU;
   GemmCfg best{0, 1, K};
   double best_t = 1e300;
-  for (int tc = 0; tc < NUM_TILE_CFGS; ++tc) {
+  // a near tie (within 0.5%) keeps the configuration met first: the one
+  // with more resident blocks, then the smaller split
+  for (int tc = NUM_TILE_CFGS - 1; tc >= 0; --tc) {
     if (deep_only && kTileCfgs[tc].bk != 32) continue;
     const TileCfg& c = kTileCfgs[tc];
     const int bm = 32 * c.mb * c.wm, bn = 32 * c.nb * c.wn, bk = c.bk;
@@ -596,9 +638,9 @@ GemmCfg choose_config(int M, int N, int K, bool akc, bool bkc, bool may_split) {
       if ((K + ks - 1) / ks != s) continue;
       if (s > 1 && (double)s * M * N * sizeof(float) > (double)MAX_SPLIT_WS) continue;
       // time in 128 x 128 x 16 tile steps of a full CU
-      const double work = (double)bm * bn / (128.0 * 128.0) * ks / 16.0 / ((akc || bkc) ? c.rate_kc : c.rate_mn);
-      double t = launch_time(tiles * s, c.occ * 4 / (c.wm * c.wn), c.wm * c.wn, work);
-      if (s > 1) t += 4.0 * (double)s * M * N / (128.0 * 128.0) / NUM_CU;  // partial tiles out and back
+      const double work =
+          (double)bm * bn / (128.0 * 128.0) * (ks / 16.0 / ((akc || bkc) ? c.rate_kc : c.rate_mn) + c.ovh);
+      const double t = launch_time(c, tiles * s, work);
       if (t < best_t * 0.995) {
         best_t = t;
         best = GemmCfg{tc, s, ks};
@@ -749,7 +791,7 @@ bt_status gemm_segmented_batched(int M, int N, int K, const float* A, int lda, l
 using namespace bt;
 
 extern "C" size_t bt_gemm_ws_bytes(bt_op opA, bt_op opB, int M, int N, int K, bt_epi epi) {
-  if (M <= 0 || N <= 0 || K <= 0 || epi != BT_EPI_NONE) return 0;
+  if (M <= 0 || N <= 0 || K <= 0 || epi < BT_EPI_NONE || epi > BT_EPI_DGELU) return 0;
   const GemmCfg c = choose_config(M, N, K, opA == BT_OP_N, opB == BT_OP_T, true);
   const int splits = c.splits;
   if (splits <= 1) return 0;
@@ -802,10 +844,9 @@ extern "C" bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K, const fl
   p.N = N;
   p.K = K;
   p.beta = beta;
-  const bool may_split = epi == BT_EPI_NONE && residual == nullptr;
   const bool akc = opA == BT_OP_N;
   const bool bkc = opB == BT_OP_T;
-  const GemmCfg cfg = choose_config(M, N, K, akc, bkc, may_split);
+  const GemmCfg cfg = choose_config(M, N, K, akc, bkc, true);
   const TileCfg& tcf = kTileCfgs[cfg.tc];
   const int bm = 32 * tcf.mb * tcf.wm, bn = 32 * tcf.nb * tcf.wn;
   p.tiles_m = (M + bm - 1) / bm;
@@ -837,8 +878,14 @@ extern "C" bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K, const fl
     const long long n4 = (long long)M * (N / 4);
     long long nb = (n4 + 255) / 256;
     if (nb > 4096) nb = 4096;
-    hipLaunchKernelGGL(splitk_reduce, dim3((unsigned)nb), dim3(256), 0, s, p.ws, C, (long long)ldc, M,
-                       N, splits, beta);
+    switch (epi) {
+      case BT_EPI_NONE: hipLaunchKernelGGL(splitk_reduce<BT_EPI_NONE>, dim3((unsigned)nb), dim3(256), 0, s, p); break;
+      case BT_EPI_BIAS: hipLaunchKernelGGL(splitk_reduce<BT_EPI_BIAS>, dim3((unsigned)nb), dim3(256), 0, s, p); break;
+      case BT_EPI_BIAS_GELU:
+        hipLaunchKernelGGL(splitk_reduce<BT_EPI_BIAS_GELU>, dim3((unsigned)nb), dim3(256), 0, s, p);
+        break;
+      default: hipLaunchKernelGGL(splitk_reduce<BT_EPI_DGELU>, dim3((unsigned)nb), dim3(256), 0, s, p); break;
+    }
     BT_TRY(check_launch("splitk_reduce"));
     if (colsum_B) {
       hipLaunchKernelGGL(splitk_colsum_reduce, dim3((N + 255) / 256), dim3(256), 0, s, p.ws_colsum, colsum_B, N,

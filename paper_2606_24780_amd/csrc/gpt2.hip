@@ -99,9 +99,15 @@ size_t scratch_need(const bt_gpt2_config& c, int B, int T) {
   const int M = B * T, C = c.C, F = 4 * c.C;
   size_t s = 0;
   auto mx = [&](size_t v) { s = v > s ? v : s; };
-  // every product of the step without an epilogue may be split along K; the
-  // split count depends on the token count, so cover every call size <= M
+  // every product of the step may be split along K (an epilogue then runs in
+  // the reduction); the split count depends on the token count, so cover
+  // every call size <= M
   for (int m = M; m >= 1; m = m > 1 ? (m + 1) / 2 : 0) {
+    mx(bt_gemm_ws_bytes(BT_OP_N, BT_OP_N, m, 3 * C, C, BT_EPI_BIAS));
+    mx(bt_gemm_ws_bytes(BT_OP_N, BT_OP_N, m, C, C, BT_EPI_BIAS));
+    mx(bt_gemm_ws_bytes(BT_OP_N, BT_OP_N, m, F, C, BT_EPI_BIAS_GELU));
+    mx(bt_gemm_ws_bytes(BT_OP_N, BT_OP_N, m, C, F, BT_EPI_BIAS));
+    mx(bt_gemm_ws_bytes(BT_OP_N, BT_OP_T, m, F, C, BT_EPI_DGELU));
     mx(bt_gemm_ws_bytes(BT_OP_T, BT_OP_N, C, 3 * C, m, BT_EPI_NONE));
     mx(bt_gemm_ws_bytes(BT_OP_T, BT_OP_N, C, C, m, BT_EPI_NONE));
     mx(bt_gemm_ws_bytes(BT_OP_T, BT_OP_N, C, F, m, BT_EPI_NONE));

@@ -84,6 +84,11 @@ def test_gemm_validation(lib):
     need = lib.bt_gemm_ws_bytes(1, 0, 768, 768, 16384, 0)
     assert need > 0
     assert _gemm(lib, opA=1, M=768, N=768, K=16384, lda=768, ldb=768, ldc=768) == BT_EWORKSPACE
+    # an epilogue product with a long K splits too (the epilogue runs in the reduction)
+    need = lib.bt_gemm_ws_bytes(0, 0, 256, 256, 4096, 1)
+    assert need > 0
+    assert _gemm(lib, M=256, N=256, K=4096, lda=4096, ldb=256, ldc=256, epi=1, bias=FAKE + 4096, ws=FAKE + 8192,
+                 wsb=need - 1) == BT_EWORKSPACE
     assert _gemm(lib, M=0) == BT_OK                  # empty product: nothing to do
 
 

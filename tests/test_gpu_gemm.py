@@ -79,16 +79,49 @@ def test_gemm_epilogues(M, N, K):
     assert np.array_equal(host(C), np.broadcast_to(bias[:8].astype(np.float64), (8, 8)))
 
 
+# Long K over few tiles splits the product; the epilogue (with residual and
+# beta = 1) then runs in the reduction of the partials.  (260, 196, 4100)
+# is ragged, (256, 256, 4096) takes the direct-copy tiles.
+@pytest.mark.parametrize("M,N,K", [(260, 196, 4100), (256, 256, 4096)])
+def test_gemm_epilogues_split(M, N, K):
+    torch = torch_gpu()
+    L = bt.lib()
+    for epi in (bt.EPI_BIAS, bt.EPI_BIAS_GELU):
+        assert L.bt_gemm_ws_bytes(0, 0, M, N, K, epi) > 0, "shape expected to split"
+    assert L.bt_gemm_ws_bytes(0, 1, M, N, K, bt.EPI_DGELU) > 0, "shape expected to split"
+    A, B = _operands(M, N, K, 0, 0)
+    bias = RNG.standard_normal(N).astype(np.float32)
+    res = RNG.standard_normal((M, N)).astype(np.float32)
+    gin = (RNG.standard_normal((M, N)) * 2).astype(np.float32)
+    C0 = RNG.standard_normal((M, N)).astype(np.float32)
+    ref = ops.gemm(A, B)
+    say(f"split gemm BIAS + residual + beta=1 M={M} N={N} K={K}")
+    C = _run(torch, 0, 0, M, N, K, A, B, bias=dev(torch, bias), epi=bt.EPI_BIAS, residual=dev(torch, res),
+             C0=C0, beta=1.0)
+    assert_close_maxabs(host(C), ref + bias + res + C0, TOL, "split bias+residual+beta")
+    say("split gemm BIAS_GELU + preact")
+    pre = torch.zeros((M, N), dtype=torch.float32, device="cuda")
+    C = _run(torch, 0, 0, M, N, K, A, B, bias=dev(torch, bias), epi=bt.EPI_BIAS_GELU, preact_out=pre)
+    assert_close_maxabs(host(pre), ref + bias, TOL, "split preact")
+    assert_close_maxabs(host(C), ops.gelu_fwd(ref + bias), TOL, "split gelu(pre)")
+    say("split gemm DGELU")
+    C = _run(torch, 0, 1, M, N, K, A, np.ascontiguousarray(B.T), epi=bt.EPI_DGELU, gelu_in=dev(torch, gin))
+    assert_close_maxabs(host(C), ref * ops.gelu_grad(gin), TOL, "split dgelu")
+
+
 @pytest.mark.parametrize("ta,tb", [(0, 0), (0, 1), (1, 0), (1, 1)])
 def test_gemm_full_tiles_match_ragged_path(ta, tb):
     """A full-tile product (direct LDS copies) and the same data inside a
     ragged product (register staging) add the same terms in the same order,
-    so the shared 256 x 256 block of C is bitwise equal.  A zero bias keeps
-    both products from being split along K (the split count could differ
-    between the two shapes) and adds exactly 0."""
+    so the shared 256 x 256 block of C is bitwise equal.  Both shapes must be
+    split along K the same way (asserted from their workspace sizes); the
+    zero bias adds exactly 0."""
     torch = torch_gpu()
     say(f"gemm full vs ragged path ta={ta} tb={tb}")
     M, N, K = 256, 256, 512
+    L = bt.lib()
+    splits = [L.bt_gemm_ws_bytes(ta, tb, m, n, K, bt.EPI_BIAS) // (4 * (m * n + n)) for m, n in ((M, N), (M + 4, N + 4))]
+    assert splits[0] == splits[1], splits
     A, B = _operands(M + 4, N + 4, K, ta, tb)
     zb = torch.zeros(N + 4, dtype=torch.float32, device="cuda")
     C_big = host(_run(torch, ta, tb, M + 4, N + 4, K, A, B, bias=zb, epi=bt.EPI_BIAS))
