@@ -35,6 +35,25 @@ bt_status fill_zero(float* p, size_t n, hipStream_t s);
 bt_status sum_partials(const float* part, int nb, long long ld, int n, float* out_a, int n_a, float* out_b,
                        float beta, hipStream_t s);
 
+// Several independent sums of the shape above (same nb, ld, n, n_a, beta),
+// one per set, in as few launches as the kernel-argument budget allows
+// (each set's result is bitwise that of sum_partials).
+struct PartialSet {
+  const float* part;
+  float* out_a;
+  float* out_b;
+};
+bt_status sum_partials_batched(const PartialSet* sets /*host*/, int nsets, int nb, long long ld, int n, int n_a,
+                               float beta, hipStream_t s);
+
+// Row pass of the LayerNorm backward alone: dx exactly as bt_layernorm_bwd
+// (dx_beta 0 or 1), and one partial row of the dgamma (first C) / dbeta
+// (next C) column sums per block in part[ln_bwd_partial_rows(M, C)][2 C],
+// to be combined by sum_partials(part, nb, 2C, 2C, dgamma, C, dbeta, ...).
+int ln_bwd_partial_rows(int M, int C);
+bt_status ln_bwd_rows(const float* dy, const float* x, const float* gamma, const float* mean, const float* rstd,
+                      float* dx, float dx_beta, float* part, int M, int C, hipStream_t s);
+
 // Batch of products C_y = A_y B_y (A [M][K] row-major, B [K][N] row-major),
 // batch y < nb nh at A + (y / nh) sa_b + (y % nh) sa_h (likewise B, C), in
 // which output rows of each 128-row tile starting at m0 sum only k < m0 + 128

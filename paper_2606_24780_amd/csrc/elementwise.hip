@@ -237,12 +237,14 @@ bt_status fill_zero(float* p, size_t n, hipStream_t s) {
 
 // 256 threads = 32 columns x 8 chains; chain g sums partials g, g+8, ...
 // with 8 loads in flight, then the 8 chains are added in order.
-__global__ void __launch_bounds__(256) sum_partials_kernel(const float* __restrict__ part, int nb, long long ld,
-                                                           int n, float* out_a, int n_a, float* out_b,
-                                                           float beta) {
+// dst[c] = beta dst[c] + sum_b part[b ld + c] for the 32 columns of this
+// block: 8 groups of 32 lanes take every 8th partial row, then group 0 adds
+// the 8 group sums in order (a fixed order for any launch).
+__device__ __forceinline__ void sum_partials_cols(const float* __restrict__ part, int nb, long long ld, int n,
+                                                  float* out_a, int n_a, float* out_b, float beta, int col_block) {
   __shared__ float red[8][33];
   const int lane = threadIdx.x & 31, g = threadIdx.x >> 5;
-  const int c = blockIdx.x * 32 + lane;
+  const int c = col_block * 32 + lane;
   float s = 0.f;
   if (c < n) {
     int b = g;
@@ -267,12 +269,44 @@ __global__ void __launch_bounds__(256) sum_partials_kernel(const float* __restri
   }
 }
 
+__global__ void __launch_bounds__(256) sum_partials_kernel(const float* __restrict__ part, int nb, long long ld,
+                                                           int n, float* out_a, int n_a, float* out_b,
+                                                           float beta) {
+  sum_partials_cols(part, nb, ld, n, out_a, n_a, out_b, beta, blockIdx.x);
+}
+
+constexpr int MAX_PARTIAL_SETS = 32;  // 768 bytes of kernel arguments
+struct PartialBatch {
+  PartialSet set[MAX_PARTIAL_SETS];
+};
+
+// blockIdx.y selects the set
+__global__ void __launch_bounds__(256) sum_partials_batched_kernel(const PartialBatch sets, int nb, long long ld,
+                                                                   int n, int n_a, float beta) {
+  const PartialSet& q = sets.set[blockIdx.y];
+  sum_partials_cols(q.part, nb, ld, n, q.out_a, n_a, q.out_b, beta, blockIdx.x);
+}
+
 bt_status sum_partials(const float* part, int nb, long long ld, int n, float* out_a, int n_a, float* out_b,
                        float beta, hipStream_t s) {
   if (n <= 0) return BT_OK;
   hipLaunchKernelGGL(sum_partials_kernel, dim3((n + 31) / 32), dim3(256), 0, s, part, nb, ld, n, out_a, n_a, out_b,
                      beta);
   return check_launch("sum_partials_kernel");
+}
+
+bt_status sum_partials_batched(const PartialSet* sets, int nsets, int nb, long long ld, int n, int n_a, float beta,
+                               hipStream_t s) {
+  if (n <= 0) return BT_OK;
+  for (int k0 = 0; k0 < nsets; k0 += MAX_PARTIAL_SETS) {
+    const int k = nsets - k0 < MAX_PARTIAL_SETS ? nsets - k0 : MAX_PARTIAL_SETS;
+    PartialBatch pb{};
+    for (int i = 0; i < k; ++i) pb.set[i] = sets[k0 + i];
+    hipLaunchKernelGGL(sum_partials_batched_kernel, dim3((n + 31) / 32, k), dim3(256), 0, s, pb, nb, ld, n, n_a,
+                       beta);
+    BT_TRY(check_launch("sum_partials_batched_kernel"));
+  }
+  return BT_OK;
 }
 
 bt_status launch_loss_sum(const float* rows, int n, float scale, int accumulate, float* d_loss, hipStream_t s) {

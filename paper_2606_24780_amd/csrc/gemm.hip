@@ -216,13 +216,12 @@ __device__ __forceinline__ floatx4 read_frag(const float* __restrict__ s, int ro
 // store: C may alias nothing, but the compiler cannot know that, and
 // interleaved load/store pairs would serialise on memory latency.
 template <int EPI>
-__device__ __forceinline__ void epilogue_block(const GemmParams& p, const floatx16& acc, int i0, int j, int hh) {
+__device__ __forceinline__ void epilogue_block(const GemmParams& p, const floatx16& acc, int i0, int j, int hh,
+                                               float bj) {
   if (j >= p.N) return;
   const bool has_res = p.residual != nullptr;
   const bool has_old = p.beta != 0.f;
-  float bj = 0.f;
-  if (EPI == BT_EPI_BIAS || EPI == BT_EPI_BIAS_GELU) bj = p.bias[j];
-  constexpr int EC = 4;  // rows whose inputs are loaded together
+  constexpr int EC = 4;  // rows whose inputs are loaded together (more spill at 4 waves per SIMD)
 #pragma unroll
   for (int r0 = 0; r0 < 16; r0 += EC) {
     float gin[EC], res[EC], old[EC];
@@ -254,6 +253,52 @@ __device__ __forceinline__ void epilogue_block(const GemmParams& p, const floatx
       }
       v += res[e] + old[e];
       p.C[off] = v;
+    }
+  }
+}
+
+// GELU-backward inputs (pre-activations, with the output's leading
+// dimension) of accumulator block b of a wave tile: 16 per lane, in
+// accumulator register order, 0 outside the matrix.
+template <int NB>
+__device__ __forceinline__ void load_gin_block(const GemmParams& p, int b, int im, int jn, int lr, int hh,
+                                               float (&g)[16]) {
+  const int j = jn + (b % NB) * 32 + lr;
+  const int i0 = im + (b / NB) * 32;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int i = i0 + 8 * (r >> 2) + 4 * hh + (r & 3);
+    g[r] = (j < p.N && i < p.M) ? p.gelu_in[(long long)i * p.ldc + j] : 0.f;
+  }
+}
+
+// Epilogue of a whole wave tile with neither a residual nor an old C to add
+// (plain, bias and GELU-backward products).  The only loads are the
+// GELU-backward inputs, read a 32 x 32 block at a time one block ahead of
+// the stores: loads and stores retire in order on one counter, so waiting
+// for inputs issued after a block's stores would also wait for those stores
+// to be written (the general path's 4-row groups do exactly that).
+template <int EPI, int MB, int NB>
+__device__ __forceinline__ void epilogue_plain(const GemmParams& p, const floatx16 (&acc)[MB][NB], int im, int jn,
+                                               int lr, int hh, const float (&bj)[NB]) {
+  constexpr int NBLK = MB * NB;
+  float gin[2][16];
+  if (EPI == BT_EPI_DGELU) load_gin_block<NB>(p, 0, im, jn, lr, hh, gin[0]);
+#pragma unroll
+  for (int b = 0; b < NBLK; ++b) {
+    if (EPI == BT_EPI_DGELU && b + 1 < NBLK) load_gin_block<NB>(p, b + 1, im, jn, lr, hh, gin[(b + 1) & 1]);
+    const int mb = b / NB, nb = b % NB;
+    const int j = jn + nb * 32 + lr;
+    if (j >= p.N) continue;
+    const int i0 = im + mb * 32;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int i = i0 + 8 * (r >> 2) + 4 * hh + (r & 3);
+      if (i >= p.M) continue;
+      float v = acc[mb][nb][r];
+      if (EPI == BT_EPI_BIAS) v += bj[nb];
+      if (EPI == BT_EPI_DGELU) v *= gelu_grad_f(gin[b & 1][r]);
+      p.C[(long long)i * p.ldc + j] = v;
     }
   }
 }
@@ -341,6 +386,14 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
   // k offset (from kbeg) of k-tile t
   auto koff = [&](int t) { return BMODE == 2 ? (t < n0t ? t * BK : p.seg + (t - n0t) * BK) : t * BK; };
 
+  // bias of this lane's output columns, loaded before the k-loop so that
+  // the epilogue never waits for it behind its own stores
+  float bias_j[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int j = n0 + wn * WTN + nb * 32 + lr;
+    bias_j[nb] = ((EPI == BT_EPI_BIAS || EPI == BT_EPI_BIAS_GELU) && !SPLIT && j < p.N) ? p.bias[j] : 0.f;
+  }
   floatx16 acc[MB][NB];
 #pragma unroll
   for (int a = 0; a < MB; ++a)
@@ -486,6 +539,14 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
 
   // ---- epilogue.  Accumulator element r of lane (lr, hh) of block (mb, nb):
   // row = 8 (r/4) + 4 hh + r%4, column = lr.
+  // Products with a residual or an old C, and the bias + GELU products
+  // (which also store the pre-activation), take the general path: a
+  // second streamed input or the GELU arithmetic there spills at 4 waves
+  // per SIMD.
+  if (!SPLIT && EPI != BT_EPI_BIAS_GELU && p.residual == nullptr && p.beta == 0.f) {
+    epilogue_plain<EPI, MB, NB>(p, acc, m0 + wm * WTM, n0 + wn * WTN, lr, hh, bias_j);
+    return;
+  }
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -500,7 +561,7 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
           if (i < p.M) p.ws[(long long)z * p.M * p.N + (long long)i * p.N + j] = acc[mb][nb][r];
         }
       } else {
-        epilogue_block<EPI>(p, acc[mb][nb], i0, j, hh);
+        epilogue_block<EPI>(p, acc[mb][nb], i0, j, hh, bias_j[nb]);
       }
     }
 }
@@ -515,6 +576,16 @@ __global__ void __launch_bounds__(256) splitk_reduce(const GemmParams p) {
   const int M = p.M, N = p.N, splits = p.splits;
   const long long n4 = (long long)M * (N / 4);
   const long long MN = (long long)M * N;
+  // column sums of op(B) (bias gradient): colsum = sum_z ws_colsum[z] +
+  // beta colsum, in the same fixed order
+  if (p.colsum != nullptr) {
+    for (int n = blockIdx.x * blockDim.x + threadIdx.x; n < N; n += gridDim.x * blockDim.x) {
+      float s = p.ws_colsum[n];
+      for (int z = 1; z < splits; ++z) s += p.ws_colsum[(long long)z * N + n];
+      if (p.beta != 0.f) s += p.colsum[n];
+      p.colsum[n] = s;
+    }
+  }
   for (long long e = (long long)blockIdx.x * blockDim.x + threadIdx.x; e < n4;
        e += (long long)gridDim.x * blockDim.x) {
     const int i = (int)(e / (N / 4));
@@ -550,16 +621,6 @@ __global__ void __launch_bounds__(256) splitk_reduce(const GemmParams p) {
   }
 }
 
-// colsum = sum_z ws_colsum[z] + beta * colsum, fixed order.
-__global__ void __launch_bounds__(256) splitk_colsum_reduce(const float* __restrict__ part, float* __restrict__ out,
-                                                            int N, int splits, float beta) {
-  const int n = blockIdx.x * blockDim.x + threadIdx.x;
-  if (n >= N) return;
-  float s = part[n];
-  for (int z = 1; z < splits; ++z) s += part[(long long)z * N + n];
-  if (beta != 0.f) s += out[n];
-  out[n] = s;
-}
 
 // Block-tile configurations: tile depth, wave grid (64 x 64 outputs per
 // wave), 32 x 32 blocks per wave, resident blocks per CU (= waves per SIMD
@@ -887,11 +948,6 @@ extern "C" bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K, const fl
       default: hipLaunchKernelGGL(splitk_reduce<BT_EPI_DGELU>, dim3((unsigned)nb), dim3(256), 0, s, p); break;
     }
     BT_TRY(check_launch("splitk_reduce"));
-    if (colsum_B) {
-      hipLaunchKernelGGL(splitk_colsum_reduce, dim3((N + 255) / 256), dim3(256), 0, s, p.ws_colsum, colsum_B, N,
-                         splits, beta);
-      BT_TRY(check_launch("splitk_colsum_reduce"));
-    }
   }
   return BT_OK;
 }

@@ -90,6 +90,7 @@ struct Layout {
   size_t per_layer;                                                      // stride between layers
   size_t resL, lnf, muf, rsf, logits, loss_rows, lse_rows;
   size_t dres, dbig, dsmall;
+  size_t ln_part, ln_part_slab;  // LayerNorm-backward partial rows: 2L+1 slabs of ln_part_slab floats
   size_t scalars;  // [loss, norm, coef, pad]
   size_t scratch, scratch_bytes;
   size_t total;
@@ -163,6 +164,8 @@ Layout make_layout(const bt_gpt2_config& c, int B, int T) {
   o.dres = take(M * C);
   o.dbig = take(M * (F > 3 * C ? F : 3 * C));
   o.dsmall = take(M * C);
+  o.ln_part_slab = align_up((size_t)ln_bwd_partial_rows((int)M, (int)C) * 2 * C, 64);
+  o.ln_part = take(o.ln_part_slab * (2 * (size_t)c.L + 1));
   o.scalars = take(64);
   o.scratch_bytes = scratch_need(c, B, T);
   o.scratch = off;
@@ -466,8 +469,18 @@ extern "C" bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, floa
                  nullptr, nullptr, nullptr, scr, scrb, s));  // dlnf
   BT_PROF(BT_PROF_GEMM, gemm_f(fV, fC, fM), gemm_b(fV, fC, fM, accumulate), bt_gemm(BT_OP_T, BT_OP_N, Vp, C, M, dlogits, Vp, lnf, C, beta, G + po.wte, C, nullptr, BT_EPI_NONE, nullptr,
                  nullptr, nullptr, nullptr, scr, scrb, s));  // dwte (LM head part)
-  BT_PROF(BT_PROF_LN_BWD, 0, ln_bwd_b0, bt_layernorm_bwd(dsm, sb.res(L), P + po.lnfg, sb.f(ly.muf), sb.f(ly.rsf), dres, G + po.lnfg, G + po.lnfb, 0.f,
-                          beta, scr, scrb, M, C, s));
+  // LayerNorm backward: dx now, the dgamma / dbeta partial rows of all 2L+1
+  // LayerNorms into their own slabs, summed by one batched launch after the
+  // last of them (each sum in the fixed order of bt_layernorm_bwd's)
+  std::vector<PartialSet> ln_sets;
+  ln_sets.reserve(2 * L + 1);
+  auto ln_bwd = [&](const float* dy, const float* x, const float* gam, const float* mu, const float* rs, float dx_beta,
+                    float* dgam, float* dbet) {
+    float* part = sb.f(ly.ln_part) + ln_sets.size() * ly.ln_part_slab;
+    ln_sets.push_back(PartialSet{part, dgam, dbet});
+    return ln_bwd_rows(dy, x, gam, mu, rs, dres, dx_beta, part, M, C, s);
+  };
+  BT_PROF(BT_PROF_LN_BWD, 0, ln_bwd_b0, ln_bwd(dsm, sb.res(L), P + po.lnfg, sb.f(ly.muf), sb.f(ly.rsf), 0.f, G + po.lnfg, G + po.lnfb));
   for (int l = L - 1; l >= 0; --l) {
     const LayerOffs& w = po.layer[l];
     float* ln1 = sb.layer(ly.ln1, l);
@@ -488,8 +501,7 @@ extern "C" bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, floa
                    nullptr, nullptr, G + w.bfc, scr, scrb, s));
     BT_PROF(BT_PROF_GEMM, gemm_f(fM, fC, fF), gemm_b(fM, fC, fF, 0), bt_gemm(BT_OP_N, BT_OP_T, M, C, F, dbig, F, P + w.Wfc, F, 0.f, dsm, C, nullptr, BT_EPI_NONE, nullptr,
                    nullptr, nullptr, nullptr, scr, scrb, s));
-    BT_PROF(BT_PROF_LN_BWD, 0, ln_bwd_b1, bt_layernorm_bwd(dsm, xmid, P + w.ln2g, sb.layer(ly.mu2, l), sb.layer(ly.rs2, l), dres, G + w.ln2g,
-                            G + w.ln2b, 1.f, beta, scr, scrb, M, C, s));
+    BT_PROF(BT_PROF_LN_BWD, 0, ln_bwd_b1, ln_bwd(dsm, xmid, P + w.ln2g, sb.layer(ly.mu2, l), sb.layer(ly.rs2, l), 1.f, G + w.ln2g, G + w.ln2b));
     // attention output projection: dWo += att^T dres with dbo ; datt = dres Wo^T
     BT_PROF(BT_PROF_GEMM, gemm_f(fC, fC, fM), gemm_b(fC, fC, fM, accumulate), bt_gemm(BT_OP_T, BT_OP_N, C, C, M, att, C, dres, C, beta, G + w.Wo, C, nullptr, BT_EPI_NONE, nullptr,
                    nullptr, nullptr, G + w.bo, scr, scrb, s));
@@ -501,9 +513,9 @@ extern "C" bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, floa
                    nullptr, nullptr, nullptr, G + w.bqkv, scr, scrb, s));
     BT_PROF(BT_PROF_GEMM, gemm_f(fM, fC, 3 * fC), gemm_b(fM, fC, 3 * fC, 0), bt_gemm(BT_OP_N, BT_OP_T, M, C, 3 * C, dbig, 3 * C, P + w.Wqkv, 3 * C, 0.f, dsm, C, nullptr, BT_EPI_NONE,
                    nullptr, nullptr, nullptr, nullptr, scr, scrb, s));
-    BT_PROF(BT_PROF_LN_BWD, 0, ln_bwd_b1, bt_layernorm_bwd(dsm, sb.res(l), P + w.ln1g, sb.layer(ly.mu1, l), sb.layer(ly.rs1, l), dres, G + w.ln1g,
-                            G + w.ln1b, 1.f, beta, scr, scrb, M, C, s));
+    BT_PROF(BT_PROF_LN_BWD, 0, ln_bwd_b1, ln_bwd(dsm, sb.res(l), P + w.ln1g, sb.layer(ly.mu1, l), sb.layer(ly.rs1, l), 1.f, G + w.ln1g, G + w.ln1b));
   }
+  BT_PROF(BT_PROF_LN_BWD, 0, 0, sum_partials_batched(ln_sets.data(), (int)ln_sets.size(), ln_bwd_partial_rows(M, C), 2LL * C, 2 * C, C, beta, s));
   BT_PROF(BT_PROF_EMB_BWD, 0, f4 * (2 * fM * fC + 2 * (double)T * fC), bt_embedding_bwd(tokens, dres, G + po.wte, G + po.wpe, beta, scr, scrb, B, T, C, Vp, s));
   // rows of wpe beyond T receive no gradient in this micro-step
   if (T < cf.max_T && !accumulate) {

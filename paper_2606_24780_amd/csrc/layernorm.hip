@@ -262,6 +262,21 @@ bt_status ln_check(int M, int C, const char* who) {
 }
 
 }  // namespace
+
+int ln_bwd_partial_rows(int M, int C) { return M > 0 ? ln_bwd_blocks(M, ln_bwd_waves(C)) : 0; }
+
+bt_status ln_bwd_rows(const float* dy, const float* x, const float* gamma, const float* mean, const float* rstd,
+                      float* dx, float dx_beta, float* part, int M, int C, hipStream_t s) {
+  BT_TRY(ln_check(M, C, "ln_bwd_rows"));
+  if (M == 0) return BT_OK;
+  const int nb = ln_bwd_partial_rows(M, C);
+  const int rpb = (M + nb - 1) / nb;
+#define BT_LN_BWD(NV) hipLaunchKernelGGL(ln_bwd_kernel<NV>, dim3(nb), dim3(64 * BwdWaves<NV>::value), 0, s, dy, x, gamma, mean, rstd, dx, part, M, C, rpb, dx_beta)
+  BT_LN_DISPATCH(ln_nv(C), BT_LN_BWD)
+#undef BT_LN_BWD
+  return check_launch("ln_bwd_kernel");
+}
+
 }  // namespace bt
 
 using namespace bt;
@@ -313,12 +328,7 @@ extern "C" bt_status bt_layernorm_bwd(const float* dy, const float* x, const flo
   const size_t need = bt_layernorm_bwd_ws_bytes(M, C);
   BT_RETURN_IF(!ws || ws_bytes < need, BT_EWORKSPACE, "bt_layernorm_bwd: workspace of %zu bytes needed (got %zu)",
                need, ws_bytes);
-  const int nb = ln_bwd_blocks(M, ln_bwd_waves(C));
-  const int rpb = (M + nb - 1) / nb;
   float* part = static_cast<float*>(ws);
-#define BT_LN_BWD(NV) hipLaunchKernelGGL(ln_bwd_kernel<NV>, dim3(nb), dim3(64 * BwdWaves<NV>::value), 0, s, dy, x, gamma, mean, rstd, dx, part, M, C, rpb, dx_beta)
-  BT_LN_DISPATCH(ln_nv(C), BT_LN_BWD)
-#undef BT_LN_BWD
-  BT_TRY(check_launch("ln_bwd_kernel"));
-  return sum_partials(part, nb, 2LL * C, 2 * C, dgamma, C, dbeta, param_beta, s);
+  BT_TRY(ln_bwd_rows(dy, x, gamma, mean, rstd, dx, dx_beta, part, M, C, s));
+  return sum_partials(part, ln_bwd_partial_rows(M, C), 2LL * C, 2 * C, dgamma, C, dbeta, param_beta, s);
 }
