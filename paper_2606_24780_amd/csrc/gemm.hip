@@ -303,6 +303,45 @@ __device__ __forceinline__ void epilogue_plain(const GemmParams& p, const floatx
   }
 }
 
+// Epilogue of a whole wave tile of a bias product with at most one tensor to
+// add, `src` (a residual, or C itself when beta = 1; null: none), streamed
+// like the GELU-backward inputs above (every element of C is read before it
+// is written).
+template <int MB, int NB>
+__device__ __forceinline__ void epilogue_bias_add(const GemmParams& p, const float* src,
+                                                  const floatx16 (&acc)[MB][NB], int im, int jn, int lr, int hh,
+                                                  const float (&bj)[NB]) {
+  constexpr int NBLK = MB * NB;
+  const bool has_in = src != nullptr;
+  float in[2][16];
+  auto load = [&](int b, float(&g)[16]) {
+    const int j = jn + (b % NB) * 32 + lr;
+    const int i0 = im + (b / NB) * 32;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int i = i0 + 8 * (r >> 2) + 4 * hh + (r & 3);
+      g[r] = (j < p.N && i < p.M) ? src[(long long)i * p.ldc + j] : 0.f;
+    }
+  };
+  if (has_in) load(0, in[0]);
+#pragma unroll
+  for (int b = 0; b < NBLK; ++b) {
+    if (has_in && b + 1 < NBLK) load(b + 1, in[(b + 1) & 1]);
+    const int mb = b / NB, nb = b % NB;
+    const int j = jn + nb * 32 + lr;
+    if (j >= p.N) continue;
+    const int i0 = im + mb * 32;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int i = i0 + 8 * (r >> 2) + 4 * hh + (r & 3);
+      if (i >= p.M) continue;
+      float v = acc[mb][nb][r] + bj[nb];
+      if (has_in) v += in[b & 1][r];
+      p.C[(long long)i * p.ldc + j] = v;
+    }
+  }
+}
+
 // WM x WN waves, each owning a (32 MB) x (32 NB) output sub-tile of MB x NB
 // MFMA accumulators: block tile (32 MB WM) x (32 NB WN), 64 WM WN threads.  DTL: every tile of the launch is
 // full (M, N multiples of the block tile, K range a multiple of BK), and
@@ -539,11 +578,21 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
 
   // ---- epilogue.  Accumulator element r of lane (lr, hh) of block (mb, nb):
   // row = 8 (r/4) + 4 hh + r%4, column = lr.
-  // Products with a residual or an old C, and the bias + GELU products
-  // (which also store the pre-activation), take the general path: a
-  // second streamed input or the GELU arithmetic there spills at 4 waves
-  // per SIMD.
-  if (!SPLIT && EPI != BT_EPI_BIAS_GELU && p.residual == nullptr && p.beta == 0.f) {
+  // Streamed epilogues: plain and GELU-backward products without additive
+  // inputs, and bias products with at most one additive input (residual or
+  // beta = 1, chosen at run time).  The rest (two additive inputs, additive
+  // inputs on the other epilogues, and the bias + GELU products, which also
+  // store the pre-activation) take the general path: streaming there spills
+  // at 4 waves per SIMD, and a run-time input on the plain products measured
+  // 1-4% slower.
+  if constexpr (!SPLIT && EPI == BT_EPI_BIAS) {
+    if (p.residual == nullptr || p.beta == 0.f) {
+      const float* src = p.residual ? p.residual : (p.beta != 0.f ? p.C : nullptr);
+      epilogue_bias_add<MB, NB>(p, src, acc, m0 + wm * WTM, n0 + wn * WTN, lr, hh, bias_j);
+      return;
+    }
+  }
+  if (!SPLIT && EPI != BT_EPI_BIAS && EPI != BT_EPI_BIAS_GELU && p.residual == nullptr && p.beta == 0.f) {
     epilogue_plain<EPI, MB, NB>(p, acc, m0 + wm * WTM, n0 + wn * WTN, lr, hh, bias_j);
     return;
   }

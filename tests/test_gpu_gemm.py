@@ -79,6 +79,55 @@ def test_gemm_epilogues(M, N, K):
     assert np.array_equal(host(C), np.broadcast_to(bias[:8].astype(np.float64), (8, 8)))
 
 
+# Every combination of epilogue and additive inputs in the tile epilogue
+# (products that are not split): the plain GELU-backward, bias and residual /
+# beta = 1 products stream their one input a block ahead of the stores; two
+# inputs and the bias + GELU products take the general 4-row path.  Ragged
+# (260, 196, 36) and full-tile (256, 256, 64) shapes, each in both B layouts.
+@pytest.mark.parametrize("M,N,K", [(260, 196, 36), (256, 256, 64)])
+@pytest.mark.parametrize("tb", [0, 1])
+def test_gemm_tile_epilogue_combinations(M, N, K, tb):
+    torch = torch_gpu()
+    L = bt.lib()
+    for epi in (bt.EPI_NONE, bt.EPI_BIAS, bt.EPI_BIAS_GELU, bt.EPI_DGELU):
+        assert L.bt_gemm_ws_bytes(0, tb, M, N, K, epi) == 0, "shape must not be split"
+    A, B = _operands(M, N, K, 0, tb)
+    bias = RNG.standard_normal(N).astype(np.float32)
+    res = RNG.standard_normal((M, N)).astype(np.float32)
+    gin = (RNG.standard_normal((M, N)) * 2).astype(np.float32)
+    C0 = RNG.standard_normal((M, N)).astype(np.float32)
+    prod = ops.gemm(A, B, False, bool(tb))
+    for epi in (bt.EPI_NONE, bt.EPI_BIAS, bt.EPI_BIAS_GELU, bt.EPI_DGELU):
+        for with_res in (False, True):
+            for beta in (0.0, 1.0):
+                say(f"gemm tile epilogue {epi} residual={with_res} beta={beta} M={M} N={N} K={K} tb={tb}")
+                kw = dict(beta=beta, epi=epi)
+                if epi in (bt.EPI_BIAS, bt.EPI_BIAS_GELU):
+                    kw["bias"] = dev(torch, bias)
+                pre = None
+                if epi == bt.EPI_BIAS_GELU:
+                    pre = torch.zeros((M, N), dtype=torch.float32, device="cuda")
+                    kw["preact_out"] = pre
+                if epi == bt.EPI_DGELU:
+                    kw["gelu_in"] = dev(torch, gin)
+                if with_res:
+                    kw["residual"] = dev(torch, res)
+                C = _run(torch, 0, tb, M, N, K, A, B, C0=C0 if beta else None, **kw)
+                v = prod.copy()
+                if epi in (bt.EPI_BIAS, bt.EPI_BIAS_GELU):
+                    v = v + bias
+                if epi == bt.EPI_BIAS_GELU:
+                    assert_close_maxabs(host(pre), v, TOL, "preact")
+                    v = ops.gelu_fwd(v)
+                if epi == bt.EPI_DGELU:
+                    v = v * ops.gelu_grad(gin)
+                if with_res:
+                    v = v + res
+                if beta:
+                    v = v + C0
+                assert_close_maxabs(host(C), v, TOL, f"epi={epi} residual={with_res} beta={beta}")
+
+
 # Long K over few tiles splits the product; the epilogue (with residual and
 # beta = 1) then runs in the reduction of the partials.  (260, 196, 4100)
 # is ragged, (256, 256, 4096) takes the direct-copy tiles.
