@@ -1,0 +1,253 @@
+"""Summaries of rocprofv3 output for the GPT-2 124M FP32 training step (B=16, T=1024).
+
+    python -m paper_2606_24780_amd.profsum stats STATS_CSV STEPS [--command CMD]
+        kernel statistics (rocprofv3 --kernel-trace --stats) as a markdown table
+        with the GEMM class's time and fraction of the FP32 matrix peak.
+    python -m paper_2606_24780_amd.profsum traffic COPY_FETCH COPY_WRITE STEP_FETCH STEP_WRITE STEPS \
+        --stats STATS_CSV --json OUT.json --md OUT.md [--command CMD ...]
+        HBM bytes per dispatch from the FETCH_SIZE / WRITE_SIZE passes (KiB per
+        dispatch), scaled by what the same counters read for a plain 1 GiB copy:
+        the GEMM class's bytes per bt_gemm call (JSON read by bench.py) and the
+        memory-bound kernels' measured bytes against their algorithmic bytes.
+
+Reads only CSV files that rocprofv3 wrote; runs nothing on the GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import json
+import os
+import re
+from collections import defaultdict
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+MFMA_FP32_PEAK_TFLOPS = 157.3
+HBM_PEAK_GBS = 8000.0
+
+# GPT-2 124M step at B = 16, T = 1024
+M, C, F, VP, L = 16384, 768, 3072, 50304, 12
+
+
+def gemm_products():
+    """(m, n, k, extra m*n operands read or written by the epilogue) of the
+    147 bt_gemm calls of one step, in call order."""
+    fwd = [(M, 3 * C, C, 0), (M, C, C, 1), (M, F, C, 1), (M, C, F, 1)]
+    bwd = [(F, C, M, 0), (M, F, C, 1), (C, F, M, 0), (M, C, F, 0),
+           (C, C, M, 0), (M, C, C, 0), (C, 3 * C, M, 0), (M, C, 3 * C, 0)]
+    return fwd * L + [(M, VP, C, 0), (M, C, VP, 0), (VP, C, M, 0)] + bwd * L
+
+
+def gemm_flops_per_step():
+    return sum(2.0 * m * n * k for m, n, k, _ in gemm_products())
+
+
+def gemm_bytes_per_step():
+    """A and B read once, C written once, epilogue operands (residual,
+    pre-activation) touched once."""
+    return sum(4.0 * (m * k + k * n + (1 + e) * m * n) for m, n, k, e in gemm_products())
+
+
+# algorithmic HBM bytes per dispatch of the memory-bound kernels
+LN_FWD_BYTES = 4.0 * (2 * M * C + 2 * M + 2 * C)
+# dy, x read and dx written, plus dx read by the 24 accumulating calls of the 25
+LN_BWD_BYTES = 4.0 * ((3 * M * C + 2 * M + C) + 24 * (4 * M * C + 2 * M + C)) / 25
+XENT_BYTES = 8.0 * M * VP
+P_124M = 124475904
+ADAMW_BYTES = 28.0 * P_124M
+SUMSQ_BYTES = 4.0 * P_124M
+
+
+def short_name(name: str) -> str:
+    n = re.sub(r"^void ", "", name)
+    n = n.replace("bt::(anonymous namespace)::", "")
+    n = re.sub(r"\(.*\)$", "", n) if "rocprim" not in n else "rocprim (radix sort)"
+    return n
+
+
+def kernel_class(name: str) -> str:
+    n = short_name(name)
+    if n.startswith("gemm_f32_mfma<"):
+        args = n[len("gemm_f32_mfma<"):-1].split(",")
+        return "gemm" if args[-1].strip() == "0" else "attn_bwd"
+    if n.startswith("splitk_reduce"):
+        return "gemm"
+    if n.startswith("attn_fwd"):
+        return "attn_fwd"
+    if n.startswith("attn_bwd"):
+        return "attn_bwd"
+    if n.startswith("ln_fwd"):
+        return "ln_fwd"
+    if n.startswith("ln_bwd") or n.startswith("sum_partials_batched"):
+        return "ln_bwd"
+    if n.startswith("xent"):
+        return "xent"
+    if n.startswith("adamw"):
+        return "adamw"
+    if n.startswith("sumsq") or n.startswith("norm_finish"):
+        return "grad_norm"
+    return "other"
+
+
+def read_stats(path):
+    rows = []
+    with open(path, newline="") as f:
+        for r in csv.DictReader(f):
+            rows.append(dict(name=r["Name"], calls=int(r["Calls"]), total_ns=float(r["TotalDurationNs"]),
+                             avg_ns=float(r["AverageNs"]), pct=float(r["Percentage"])))
+    return rows
+
+
+def stats_markdown(path, steps, command=None):
+    rows = read_stats(path)
+    total = sum(r["total_ns"] for r in rows)
+    out = []
+    if command:
+        out += ["Command (from the repository root on the GPU box):", "", "```", command, "```", ""]
+    out += [f"The profiled process runs {steps} training steps (warm-up + timed); per-step figures divide by "
+            f"{steps}.", "", "| kernel | calls/step | ms/step | avg us | % of GPU time |", "|---|---:|---:|---:|---:|"]
+    for r in sorted(rows, key=lambda r: -r["total_ns"]):
+        out.append(f"| `{short_name(r['name'])}` | {r['calls'] / steps:.6g} | {r['total_ns'] / steps / 1e6:.3f} | "
+                   f"{r['avg_ns'] / 1e3:.1f} | {100 * r['total_ns'] / total:.1f} |")
+    cls = defaultdict(float)
+    for r in rows:
+        cls[kernel_class(r["name"])] += r["total_ns"] / steps / 1e6
+    g_ms = cls["gemm"]
+    tf = gemm_flops_per_step() / (g_ms / 1e3) / 1e12
+    out += ["", f"Total GPU kernel time per step: {total / steps / 1e6:.2f} ms.", "",
+            "Per class (ms/step): " + ", ".join(f"{k} {v:.3f}" for k, v in sorted(cls.items(), key=lambda x: -x[1])),
+            "", "GEMM class (every `gemm_f32_mfma` instantiation with BMODE 0, i.e. the 147 `bt_gemm` products "
+            "of a step, plus their split-K reductions; the batched causal dQ product inside the attention "
+            f"backward is attention): {g_ms:.2f} ms/step; algorithmic {gemm_flops_per_step():.4e} FLOP/step -> "
+            f"{tf:.1f} TFLOP/s = {100 * tf / MFMA_FP32_PEAK_TFLOPS:.1f}% of the {MFMA_FP32_PEAK_TFLOPS} TFLOP/s "
+            "FP32 matrix peak."]
+    return "\n".join(out) + "\n"
+
+
+def read_pmc(path, counter):
+    """[(kernel name, value in KiB)] per dispatch, in dispatch order."""
+    out = []
+    with open(path, newline="") as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] == counter:
+                out.append((int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
+    out.sort()
+    return [(n, v) for _, n, v in out]
+
+
+def copy_scale(path, counter, nbytes=1 << 30):
+    """bytes per counter KiB, from the 1 GiB device copies of bench.py --calibrate-copy."""
+    vals = [v for n, v in read_pmc(path, counter) if "copyBuffer" in n and v > 0]
+    if not vals:
+        raise SystemExit(f"{path}: no copy dispatch with {counter}")
+    return nbytes / (max(vals) * 1024.0), max(vals)
+
+
+def code_sha256(path):
+    lines = []
+    for line in open(path, encoding="utf-8"):
+        line = re.sub(r"//.*$", "", line).rstrip()
+        if line:
+            lines.append(line)
+    return hashlib.sha256("\n".join(lines).encode()).hexdigest()
+
+
+def traffic(a):
+    fs, fkib = copy_scale(a.copy_fetch, "FETCH_SIZE")
+    ws, wkib = copy_scale(a.copy_write, "WRITE_SIZE")
+    fetch = read_pmc(a.step_fetch, "FETCH_SIZE")
+    write = read_pmc(a.step_write, "WRITE_SIZE")
+    by = defaultdict(lambda: [0, 0.0, 0.0])  # class -> dispatches, fetch bytes, write bytes
+    per_kernel = defaultdict(lambda: [0, 0.0, 0.0])
+    for (n, v) in fetch:
+        c = kernel_class(n)
+        by[c][0] += 1
+        by[c][1] += v * 1024 * fs
+        k = short_name(n)
+        per_kernel[k][0] += 1
+        per_kernel[k][1] += v * 1024 * fs
+    for (n, v) in write:
+        by[kernel_class(n)][2] += v * 1024 * ws
+        per_kernel[short_name(n)][2] += v * 1024 * ws
+    steps = a.steps
+    launches = 147 * steps
+    g = by["gemm"]
+    alg = gemm_bytes_per_step()
+    rec = {
+        "kernel": "gemm_f32_mfma (every bt_gemm call of the step, with its split-K reductions; not the batched "
+                  "causal dQ product inside the attention backward)",
+        "workload": "GPT-2 124M FP32 train step, B=16, T=1024 (147 products per step)",
+        "commands": a.command or [],
+        "copy_calibration": {"bytes_read": 1 << 30, "bytes_written": 1 << 30, "FETCH_SIZE_KiB": fkib,
+                             "WRITE_SIZE_KiB": wkib, "fetch_scale": round(1024 * fs, 4),
+                             "write_scale": round(1024 * ws, 4)},
+        "steps_profiled": steps,
+        "gemm_launches": launches,
+        "gemm_kernel_dispatches_counted": g[0],
+        "fetch_bytes_per_step": round(g[1] / steps),
+        "write_bytes_per_step": round(g[2] / steps),
+        "traffic_bytes_per_launch": round((g[1] + g[2]) / launches),
+        "algorithmic_bytes_per_step": round(alg),
+        "algorithmic_bytes_per_launch": round(alg / 147),
+        "gemm_source_sha256": code_sha256(os.path.join(HERE, "csrc", "gemm.hip")),
+        "sha_note": "sha256 of gemm.hip with // comments and blank lines removed (bench.py code_sha256)",
+    }
+    with open(a.json, "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+    dur = {}
+    if a.stats:
+        for r in read_stats(a.stats):
+            dur[short_name(r["name"])] = r["avg_ns"]
+    alg_per = {"ln_fwd_kernel": LN_FWD_BYTES, "ln_bwd_kernel": LN_BWD_BYTES, "xent_stream_kernel": XENT_BYTES,
+               "adamw_kernel": ADAMW_BYTES, "sumsq_kernel": SUMSQ_BYTES}
+    out = ["HBM-side bytes per dispatch from rocprofv3 `FETCH_SIZE` and `WRITE_SIZE` (separate passes), "
+           f"scaled by a plain 1 GiB copy (FETCH x {1024 * fs:.4f}, WRITE x {1024 * ws:.4f} bytes per KiB).", ""]
+    if a.command:
+        out += ["Commands (from the repository root on the GPU box):", "", "```"] + a.command + ["```", ""]
+    out += ["| kernel | dispatches/step | read MB | written MB | measured MB | algorithmic MB | measured / alg. "
+            "| avg us (stats run) | algorithmic GB/s | % of 8 TB/s |", "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
+    for k, (nd, fb, wb) in sorted(per_kernel.items(), key=lambda x: -(x[1][1] + x[1][2])):
+        base = next((b for p, b in alg_per.items() if k.startswith(p)), None)
+        if base is None:
+            continue
+        base_note = base
+        d = dur.get(k)
+        gbs = base_note / (d * 1e-9) / 1e9 if d else float("nan")
+        out.append(f"| `{k}` | {nd / steps:g} | {fb / nd / 1e6:.1f} | {wb / nd / 1e6:.1f} | {(fb + wb) / nd / 1e6:.1f} | "
+                   f"{base_note / 1e6:.1f} | {(fb + wb) / nd / base_note:.3f} | {d / 1e3 if d else float('nan'):.1f} | "
+                   f"{gbs:.0f} | {100 * gbs / HBM_PEAK_GBS:.1f} |")
+    out += ["", f"GEMM class: {g[0] / steps:g} dispatches per step (147 bt_gemm calls); "
+            f"{(g[1] + g[2]) / launches / 1e6:.1f} MB per call measured against {alg / 147 / 1e6:.1f} MB algorithmic "
+            f"({(g[1] + g[2]) / steps / alg:.2f}x)."]
+    with open(a.md, "w") as f:
+        f.write("\n".join(out) + "\n")
+    print(json.dumps({k: rec[k] for k in ("traffic_bytes_per_launch", "algorithmic_bytes_per_launch",
+                                          "gemm_kernel_dispatches_counted")}))
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("csv")
+    s.add_argument("steps", type=int)
+    s.add_argument("--command")
+    t = sub.add_parser("traffic")
+    for n in ("copy_fetch", "copy_write", "step_fetch", "step_write"):
+        t.add_argument(n)
+    t.add_argument("steps", type=int)
+    t.add_argument("--stats")
+    t.add_argument("--json", required=True)
+    t.add_argument("--md", required=True)
+    t.add_argument("--command", action="append")
+    a = ap.parse_args()
+    if a.cmd == "stats":
+        print(stats_markdown(a.csv, a.steps, a.command), end="")
+    else:
+        traffic(a)
+
+
+if __name__ == "__main__":
+    main()
