@@ -180,8 +180,8 @@ def traffic(a):
         "workload": "GPT-2 124M FP32 train step, B=16, T=1024 (147 products per step)",
         "commands": a.command or [],
         "copy_calibration": {"bytes_read": 1 << 30, "bytes_written": 1 << 30, "FETCH_SIZE_KiB": fkib,
-                             "WRITE_SIZE_KiB": wkib, "fetch_scale": round(1024 * fs, 4),
-                             "write_scale": round(1024 * ws, 4)},
+                             "WRITE_SIZE_KiB": wkib, "fetch_scale": round(fs, 4),
+                             "write_scale": round(ws, 4)},
         "steps_profiled": steps,
         "gemm_launches": launches,
         "gemm_kernel_dispatches_counted": g[0],
@@ -203,7 +203,7 @@ def traffic(a):
     alg_per = {"ln_fwd_kernel": LN_FWD_BYTES, "ln_bwd_kernel": LN_BWD_BYTES, "xent_stream_kernel": XENT_BYTES,
                "adamw_kernel": ADAMW_BYTES, "sumsq_kernel": SUMSQ_BYTES}
     out = ["HBM-side bytes per dispatch from rocprofv3 `FETCH_SIZE` and `WRITE_SIZE` (separate passes), "
-           f"scaled by a plain 1 GiB copy (FETCH x {1024 * fs:.4f}, WRITE x {1024 * ws:.4f} bytes per KiB).", ""]
+           f"scaled by a plain 1 GiB copy (counter bytes x {fs:.4f} for FETCH_SIZE, x {ws:.4f} for WRITE_SIZE).", ""]
     if a.command:
         out += ["Commands (from the repository root on the GPU box):", "", "```"] + a.command + ["```", ""]
     out += ["| kernel | dispatches/step | read MB | written MB | measured MB | algorithmic MB | measured / alg. "

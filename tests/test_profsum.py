@@ -1,0 +1,61 @@
+"""The rocprofv3 summariser (CPU): step totals of the GEMM class and the
+parsing of the statistics and counter CSVs it reads."""
+import csv
+import json
+
+from paper_2606_24780_amd import profsum
+
+
+def test_gemm_totals_match_the_step():
+    # 12 layers x 12 products + 3 LM-head products; FLOPs 2MNK summed
+    prods = profsum.gemm_products()
+    assert len(prods) == 147
+    assert profsum.gemm_flops_per_step() == 12147241254912
+    assert profsum.gemm_bytes_per_step() == 46554808320
+
+
+def _write(path, header, rows):
+    with open(path, "w", newline="") as f:
+        w = csv.writer(f, quoting=csv.QUOTE_NONNUMERIC)
+        w.writerow(header)
+        w.writerows(rows)
+
+
+PMC = ["Correlation_Id", "Dispatch_Id", "Agent_Id", "Queue_Id", "Process_Id", "Thread_Id", "Grid_Size", "Kernel_Id",
+       "Kernel_Name", "Workgroup_Size", "LDS_Block_Size", "Scratch_Size", "VGPR_Count", "Accum_VGPR_Count",
+       "SGPR_Count", "Counter_Name", "Counter_Value", "Start_Timestamp", "End_Timestamp"]
+
+
+def _pmc_row(i, name, counter, kib):
+    return [i, i, "Agent 1", 1, 1, 1, 256, 1, name, 256, 0, 0, 4, 0, 16, counter, kib, 0, 1]
+
+
+def test_stats_and_traffic_parsing(tmp_path):
+    gemm = "void bt::(anonymous namespace)::gemm_f32_mfma<true, true, 0, false, false, 16, 4, 2, 2, 2, 2, true, 0>(x)"
+    dq = "void bt::(anonymous namespace)::gemm_f32_mfma<true, false, 0, false, false, 16, 1, 2, 2, 2, 1, true, 1>(x)"
+    ln = "void bt::(anonymous namespace)::ln_fwd_kernel<3, 2>(float const*)"
+    stats = tmp_path / "s.csv"
+    _write(stats, ["Name", "Calls", "TotalDurationNs", "AverageNs", "Percentage", "MinNs", "MaxNs", "StdDev"],
+           [[gemm, 2, 2e6, 1e6, 90.0, 1, 1, 0], [dq, 2, 1e5, 5e4, 5.0, 1, 1, 0], [ln, 50, 1e5, 2e3, 5.0, 1, 1, 0]])
+    md = profsum.stats_markdown(str(stats), 2)
+    assert "`gemm_f32_mfma<true, true, 0, false, false, 16, 4, 2, 2, 2, 2, true, 0>` | 1 | 1.000 |" in md
+    assert profsum.kernel_class(dq) == "attn_bwd" and profsum.kernel_class(gemm) == "gemm"
+    # copy calibration: 1 GiB read as 524288 KiB of FETCH_SIZE (x2), written as 1048576 KiB
+    cf, cw = tmp_path / "cf.csv", tmp_path / "cw.csv"
+    _write(cf, PMC, [_pmc_row(1, "__amd_rocclr_copyBuffer", "FETCH_SIZE", 524288.0)])
+    _write(cw, PMC, [_pmc_row(1, "__amd_rocclr_copyBuffer", "WRITE_SIZE", 1048576.0)])
+    sf, sw = tmp_path / "sf.csv", tmp_path / "sw.csv"
+    _write(sf, PMC, [_pmc_row(i, ln, "FETCH_SIZE", 100.0) for i in range(50)])
+    _write(sw, PMC, [_pmc_row(i, ln, "WRITE_SIZE", 200.0) for i in range(50)])
+
+    import types
+    A = types.SimpleNamespace(copy_fetch=str(cf), copy_write=str(cw), step_fetch=str(sf), step_write=str(sw), steps=2,
+                              stats=str(stats), json=str(tmp_path / "t.json"), md=str(tmp_path / "t.md"),
+                              command=["cmd"])
+    profsum.traffic(A)
+    rec = json.load(open(A.json))
+    assert rec["copy_calibration"]["fetch_scale"] == 2.0 and rec["copy_calibration"]["write_scale"] == 1.0
+    assert rec["gemm_launches"] == 294
+    text = open(A.md).read()
+    # 100 KiB x 2048 B read and 200 KiB x 1024 B written per dispatch
+    assert "| `ln_fwd_kernel<3, 2>` | 25 | 0.2 | 0.2 | 0.4 |" in text
