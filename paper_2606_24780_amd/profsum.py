@@ -30,17 +30,19 @@ HBM_PEAK_GBS = 8000.0
 M, C, F, VP, L = 16384, 768, 3072, 50304, 12
 
 
-def gemm_products():
+def gemm_products(M=M, C=C, L=L, VP=VP):
     """(m, n, k, extra m*n operands read or written by the epilogue) of the
-    147 bt_gemm calls of one step, in call order."""
+    12 L + 3 bt_gemm calls of one step (M tokens, d_model C, MLP 4C, L
+    layers, padded vocabulary VP), in call order."""
+    F = 4 * C
     fwd = [(M, 3 * C, C, 0), (M, C, C, 1), (M, F, C, 1), (M, C, F, 1)]
     bwd = [(F, C, M, 0), (M, F, C, 1), (C, F, M, 0), (M, C, F, 0),
            (C, C, M, 0), (M, C, C, 0), (C, 3 * C, M, 0), (M, C, 3 * C, 0)]
     return fwd * L + [(M, VP, C, 0), (M, C, VP, 0), (VP, C, M, 0)] + bwd * L
 
 
-def gemm_flops_per_step():
-    return sum(2.0 * m * n * k for m, n, k, _ in gemm_products())
+def gemm_flops_per_step(**dims):
+    return sum(2.0 * m * n * k for m, n, k, _ in gemm_products(**dims))
 
 
 def gemm_bytes_per_step():
@@ -99,7 +101,7 @@ def read_stats(path):
     return rows
 
 
-def stats_markdown(path, steps, command=None):
+def stats_markdown(path, steps, command=None, **dims):
     rows = read_stats(path)
     total = sum(r["total_ns"] for r in rows)
     out = []
@@ -114,12 +116,14 @@ def stats_markdown(path, steps, command=None):
     for r in rows:
         cls[kernel_class(r["name"])] += r["total_ns"] / steps / 1e6
     g_ms = cls["gemm"]
-    tf = gemm_flops_per_step() / (g_ms / 1e3) / 1e12
+    flops = gemm_flops_per_step(**dims)
+    n_calls = len(gemm_products(**dims))
+    tf = flops / (g_ms / 1e3) / 1e12
     out += ["", f"Total GPU kernel time per step: {total / steps / 1e6:.2f} ms.", "",
             "Per class (ms/step): " + ", ".join(f"{k} {v:.3f}" for k, v in sorted(cls.items(), key=lambda x: -x[1])),
-            "", "GEMM class (every `gemm_f32_mfma` instantiation with BMODE 0, i.e. the 147 `bt_gemm` products "
-            "of a step, plus their split-K reductions; the batched causal dQ product inside the attention "
-            f"backward is attention): {g_ms:.2f} ms/step; algorithmic {gemm_flops_per_step():.4e} FLOP/step -> "
+            "", f"GEMM class (every `gemm_f32_mfma` instantiation with BMODE 0, i.e. the {n_calls} `bt_gemm` "
+            "products of a step, plus their split-K reductions; the batched causal dQ product inside the attention "
+            f"backward is attention): {g_ms:.2f} ms/step; algorithmic {flops:.4e} FLOP/step -> "
             f"{tf:.1f} TFLOP/s = {100 * tf / MFMA_FP32_PEAK_TFLOPS:.1f}% of the {MFMA_FP32_PEAK_TFLOPS} TFLOP/s "
             "FP32 matrix peak."]
     return "\n".join(out) + "\n"
@@ -234,6 +238,10 @@ def main():
     s.add_argument("csv")
     s.add_argument("steps", type=int)
     s.add_argument("--command")
+    s.add_argument("--tokens", type=int, default=M, help="B*T (default 16384)")
+    s.add_argument("--d-model", type=int, default=C)
+    s.add_argument("--layers", type=int, default=L)
+    s.add_argument("--vocab-padded", type=int, default=VP)
     t = sub.add_parser("traffic")
     for n in ("copy_fetch", "copy_write", "step_fetch", "step_write"):
         t.add_argument(n)
@@ -244,7 +252,8 @@ def main():
     t.add_argument("--command", action="append")
     a = ap.parse_args()
     if a.cmd == "stats":
-        print(stats_markdown(a.csv, a.steps, a.command), end="")
+        print(stats_markdown(a.csv, a.steps, a.command, M=a.tokens, C=a.d_model, L=a.layers, VP=a.vocab_padded),
+              end="")
     else:
         traffic(a)
 
