@@ -210,6 +210,42 @@ def test_tiny_accumulation_equals_large_batch():
                   what="accum")
 
 
+def test_deep_narrow_accumulation_vs_oracle():
+    """17 layers: the step's 35 LayerNorm dgamma / dbeta sums take two batched
+    launches (at most 32 per launch), and with two accumulating micro-steps
+    the second adds into the first's parameter gradients."""
+    torch = torch_gpu()
+    cfg = synth.GPT2Config(V=256, Vp=256, max_T=32, L=17, H=4, C=64)
+    hp = synth.HP_124M
+    specs = synth.param_specs(cfg)
+    # LayerNorm gains and biases away from 1 / 0, so that their gradients are not special
+    params = synth.init_params(cfg, 7)
+    rng = np.random.Generator(np.random.PCG64(70))
+    for name in params:
+        if name.endswith(("ln1g", "ln2g", "lnfg")):
+            params[name] = (1.0 + 0.2 * rng.standard_normal(params[name].shape)).astype(np.float32)
+        elif name.endswith(("ln1b", "ln2b", "lnfb")):
+            params[name] = (0.2 * rng.standard_normal(params[name].shape)).astype(np.float32)
+    stream = synth.zipf_tokens(4 * 32 + 1, cfg.V, 1.1, 71)
+    x, y = synth.shifted_pair(stream, 4, 32)
+    say("gpt2 deep narrow (L=17) accumulation 2 x 2 vs oracle")
+    acc = bt.GPT2(cfg, hp, 2, 32)
+    acc.load_params(synth.flatten(cfg, params))
+    d_loss = torch.zeros(1, device="cuda")
+    for k in range(2):
+        acc.fwd_bwd(dev(torch, x[2 * k:2 * k + 2]), dev(torch, y[2 * k:2 * k + 2]), 1.0 / (4 * 32), k > 0, d_loss)
+    acc.optimizer_step(1, hp.lr)
+    torch.cuda.synchronize()
+    zeros = {k: np.zeros_like(v, dtype=np.float64) for k, v in params.items()}
+    ref = og.train_step(cfg, hp, specs, params, zeros, zeros, x, y, t=1, accum=2)
+    assert abs(float(d_loss.item()) - ref["loss"]) <= LOSS_TOL * abs(ref["loss"])
+    ga = _unflat(cfg, acc.grads)
+    for name, _, _ in specs:
+        assert_close_maxabs(ga[name], ref["grads"][name], GRAD_TOL, f"deep accum vs oracle {name}")
+    _check_update(cfg, hp, specs, params, ga, _unflat(cfg, acc.params), _unflat(cfg, acc.m), _unflat(cfg, acc.v), 1,
+                  what="deep accum")
+
+
 # ---------------------------------------------------------------- GPT-2 124M
 def _inputs_124m(B=16, T=1024):
     cfg = synth.GPT2_124M
