@@ -221,7 +221,7 @@ __device__ __forceinline__ void epilogue_block(const GemmParams& p, const floatx
   if (j >= p.N) return;
   const bool has_res = p.residual != nullptr;
   const bool has_old = p.beta != 0.f;
-  constexpr int EC = 4;  // rows whose inputs are loaded together (more spill at 4 waves per SIMD)
+  constexpr int EC = 4;  // rows whose inputs are loaded together (8 or 16 spill at 4 waves per SIMD)
 #pragma unroll
   for (int r0 = 0; r0 < 16; r0 += EC) {
     float gin[EC], res[EC], old[EC];
