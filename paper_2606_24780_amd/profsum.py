@@ -3,6 +3,9 @@
     python -m paper_2606_24780_amd.profsum stats STATS_CSV STEPS [--command CMD]
         kernel statistics (rocprofv3 --kernel-trace --stats) as a markdown table
         with the GEMM class's time and fraction of the FP32 matrix peak.
+    python -m paper_2606_24780_amd.profsum ratio PMC_CSV NUM DEN FULL STEPS [--command CMD]
+        per-kernel ratio of two counters of one --pmc pass (e.g. matrix-pipe busy
+        cycles per GUI cycle, FULL being the value of a pipe busy every cycle).
     python -m paper_2606_24780_amd.profsum traffic COPY_FETCH COPY_WRITE STEP_FETCH STEP_WRITE STEPS \
         --stats STATS_CSV --json OUT.json --md OUT.md [--command CMD ...]
         HBM bytes per dispatch from the FETCH_SIZE / WRITE_SIZE passes (KiB per
@@ -231,6 +234,29 @@ def traffic(a):
                                           "gemm_kernel_dispatches_counted")}))
 
 
+def ratio_markdown(path, num, den, full, steps, command=None):
+    """Per kernel: sum of counter `num` over sum of counter `den` over its
+    dispatches (one --pmc pass holding both), and that ratio over `full`."""
+    acc = defaultdict(lambda: [0, 0.0, 0.0])
+    with open(path, newline="") as f:
+        for r in csv.DictReader(f):
+            k = short_name(r["Kernel_Name"])
+            if r["Counter_Name"] == num:
+                acc[k][1] += float(r["Counter_Value"])
+                acc[k][0] += 1
+            elif r["Counter_Name"] == den:
+                acc[k][2] += float(r["Counter_Value"])
+    out = []
+    if command:
+        out += ["Command (from the repository root on the GPU box):", "", "```", command, "```", ""]
+    out += [f"| kernel | dispatches/step | {num} / {den} | of {full:g} |", "|---|---:|---:|---:|"]
+    for k, (n, a, b) in sorted(acc.items(), key=lambda x: -x[1][2]):
+        if b <= 0 or n == 0 or a <= 0:
+            continue  # kernels that never use the counted unit
+        out.append(f"| `{k}` | {n / steps:g} | {a / b:.1f} | {100 * a / b / full:.1f}% |")
+    return "\n".join(out) + "\n"
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -250,8 +276,17 @@ def main():
     t.add_argument("--json", required=True)
     t.add_argument("--md", required=True)
     t.add_argument("--command", action="append")
+    r = sub.add_parser("ratio")
+    r.add_argument("csv")
+    r.add_argument("num")
+    r.add_argument("den")
+    r.add_argument("full", type=float)
+    r.add_argument("steps", type=int)
+    r.add_argument("--command")
     a = ap.parse_args()
-    if a.cmd == "stats":
+    if a.cmd == "ratio":
+        print(ratio_markdown(a.csv, a.num, a.den, a.full, a.steps, a.command), end="")
+    elif a.cmd == "stats":
         print(stats_markdown(a.csv, a.steps, a.command, M=a.tokens, C=a.d_model, L=a.layers, VP=a.vocab_padded),
               end="")
     else:
