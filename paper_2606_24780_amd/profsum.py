@@ -66,7 +66,7 @@ SUMSQ_BYTES = 4.0 * P_124M
 
 def short_name(name: str) -> str:
     n = re.sub(r"^void ", "", name)
-    n = n.replace("bt::(anonymous namespace)::", "")
+    n = n.replace("bt::(anonymous namespace)::", "").replace("bt::", "")
     n = re.sub(r"\(.*\)$", "", n) if "rocprim" not in n else "rocprim (radix sort)"
     return n
 
