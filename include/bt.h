@@ -323,13 +323,18 @@ size_t bt_grad_norm_ws_bytes(size_t n);
 
 /*
  * Embeddings with learned positions and the token table tied to the LM head
- * (GPT-2 architecture figure).  tokens [B, T] in [0, Vp).
+ * (GPT-2 architecture figure).  tokens [B, T] int32 (values outside [0, Vp)
+ * are clamped to that range).  C a multiple of 4, 0 < Vp <= 2^24,
+ * B*T*C/4 < 2^31; otherwise BT_ESHAPE.
  * fwd: x0[b, t, :] = wte[tokens[b, t], :] + wpe[t, :]            (x0 [B*T, C])
  * bwd: dwte[v, :] += sum over positions with token v of dx0       (always accumulates)
- *      dwpe[t, :]  = wpe_beta * dwpe[t, :] + sum_b dx0[b, t, :]    (rows t < T)
- * The backward sorts positions by token on the device and sums each token's
- * rows in position order (deterministic).  ws holds
- * bt_embedding_bwd_ws_bytes(B, T, C, Vp) bytes.  C multiple of 4.
+ *      dwpe[t, :]  = wpe_beta * dwpe[t, :] + sum_b dx0[b, t, :]    (rows t < T; wpe_beta 0 or 1)
+ * The backward groups the positions by token on the device (a token index:
+ * a stable sort of (token, position)) and adds each token's rows in position
+ * order and each position's rows in batch order: deterministic, no
+ * floating-point atomics.
+ * bt_embedding_bwd builds the index itself in ws (bt_embedding_bwd_ws_bytes
+ * bytes, 16-byte aligned, scratch): three launches.
  */
 bt_status bt_embedding_fwd(const int32_t* tokens, const float* wte, const float* wpe, float* x0,
                            int B, int T, int C, int Vp, void* stream);
@@ -337,6 +342,25 @@ bt_status bt_embedding_bwd(const int32_t* tokens, const float* dx0, float* dwte,
                            float wpe_beta, void* ws, size_t ws_bytes, int B, int T, int C, int Vp,
                            void* stream);
 size_t bt_embedding_bwd_ws_bytes(int B, int T, int C, int Vp);
+/*
+ * The backward in two halves.  bt_embedding_index builds the token index of
+ * tokens [B, T] (one workgroup: a stable radix sort of (token, position) and
+ * the run boundaries of the sorted list) into `index`, a caller-owned device
+ * buffer of bt_embedding_index_bytes(B, T) bytes, 16-byte aligned.  It only
+ * reads the tokens, so it can run on another stream while the forward runs.
+ * bt_embedding_bwd_indexed then sums dx0 as bt_embedding_bwd does (two
+ * launches; ws holds bt_embedding_bwd_indexed_ws_bytes(B, T, C) bytes of
+ * per-piece partial sums).  The index must stay unchanged until the backward
+ * has run; it may serve several backward calls on the same tokens.  Results
+ * equal bt_embedding_bwd bitwise.
+ */
+size_t bt_embedding_index_bytes(int B, int T);
+bt_status bt_embedding_index(const int32_t* tokens, void* index, size_t index_bytes, int B, int T, int Vp,
+                             void* stream);
+bt_status bt_embedding_bwd_indexed(const void* index, size_t index_bytes, const float* dx0, float* dwte,
+                                   float* dwpe, float wpe_beta, void* ws, size_t ws_bytes, int B, int T,
+                                   int C, int Vp, void* stream);
+size_t bt_embedding_bwd_indexed_ws_bytes(int B, int T, int C);
 
 /*
  * Column sums ("reduce-sum" kernel of the appendix; bias gradients):
@@ -380,8 +404,13 @@ bt_status bt_gpt2_param_offsets(const bt_gpt2_config* cfg, size_t* offsets, int*
 /* Device workspace for activations and scratch of a step with up to
  * max_B x max_T tokens. */
 size_t bt_gpt2_workspace_bytes(const bt_gpt2_config* cfg, int max_B, int max_T);
-/* Creates a host-side context bound to the caller's workspace and stream.
- * The step counter t starts at 0. */
+/* Creates a host-side context bound to the caller's workspace and stream
+ * (no HIP call).  At its first step the context creates a second HIP stream
+ * (default priority) and two events, released by bt_gpt2_destroy: each
+ * micro-step builds the embedding backward's token index on that stream
+ * while the forward runs on `stream`, forked after the work already enqueued
+ * on `stream` and joined before the embedding backward.  The step counter t
+ * starts at 0. */
 bt_status bt_gpt2_create(const bt_gpt2_config* cfg, void* workspace, size_t ws_bytes, int max_B,
                          int max_T, void* stream, bt_gpt2_ctx** out);
 /* Frees the host-side context only; never touches caller memory. */

@@ -108,6 +108,10 @@ _SIGS = {
     "bt_embedding_fwd": (i32, [vp, vp, vp, vp, i32, i32, i32, i32, vp]),
     "bt_embedding_bwd": (i32, [vp, vp, vp, vp, f32, vp, sz, i32, i32, i32, i32, vp]),
     "bt_embedding_bwd_ws_bytes": (sz, [i32, i32, i32, i32]),
+    "bt_embedding_index_bytes": (sz, [i32, i32]),
+    "bt_embedding_index": (i32, [vp, vp, sz, i32, i32, i32, vp]),
+    "bt_embedding_bwd_indexed": (i32, [vp, sz, vp, vp, vp, f32, vp, sz, i32, i32, i32, i32, vp]),
+    "bt_embedding_bwd_indexed_ws_bytes": (sz, [i32, i32, i32]),
     "bt_colsum": (i32, [vp, i32, i32, i32, vp, f32, vp, sz, vp]),
     "bt_colsum_ws_bytes": (sz, [i32, i32]),
     "bt_gpt2_num_params": (sz, [_c.POINTER(GPT2ConfigC)]),
@@ -324,6 +328,20 @@ def bt_embedding_bwd(tokens, dx0, dwte, dwpe, wpe_beta, B, T, C, Vp, ws=None, st
     _check(L.bt_embedding_bwd(_p(tokens), _p(dx0), _p(dwte), _p(dwpe), wpe_beta, _p(w),
                               0 if w is None else w.numel() * w.element_size(), B, T, C, Vp,
                               _stream(stream)), "bt_embedding_bwd")
+
+
+def bt_embedding_index(tokens, index, B, T, Vp, stream=None):
+    """index: a uint8 GPU tensor of at least bt_embedding_index_bytes(B, T) bytes."""
+    _check(lib().bt_embedding_index(_p(tokens), _p(index), index.numel(), B, T, Vp, _stream(stream)),
+           "bt_embedding_index")
+
+
+def bt_embedding_bwd_indexed(index, dx0, dwte, dwpe, wpe_beta, B, T, C, Vp, ws=None, stream=None):
+    L = lib()
+    w = _ws(L.bt_embedding_bwd_indexed_ws_bytes(B, T, C), ws, dx0.device)
+    _check(L.bt_embedding_bwd_indexed(_p(index), index.numel(), _p(dx0), _p(dwte), _p(dwpe), wpe_beta, _p(w),
+                                      0 if w is None else w.numel() * w.element_size(), B, T, C, Vp,
+                                      _stream(stream)), "bt_embedding_bwd_indexed")
 
 
 def bt_colsum(X, M, N, ldx, out, beta, ws=None, stream=None):

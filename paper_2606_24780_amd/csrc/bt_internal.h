@@ -70,6 +70,11 @@ bt_status gemm_segmented_batched(int M, int N, int K, const float* A, int lda, l
                                  long long sc_b, long long sc_h, int nb, int nh, float beta, int seg,
                                  const int* q_pos, const int* k_pos, hipStream_t stream);
 
+// Embedding backward buffers of the composed step: the token index
+// (bt_embedding_index) and the backward's run partials.
+size_t emb_index_bytes(long long M);
+size_t emb_bwd_partials_bytes(long long M, int C);
+
 // ------------------------------------------------------------------ device
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));

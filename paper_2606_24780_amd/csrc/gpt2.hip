@@ -91,6 +91,7 @@ struct Layout {
   size_t resL, lnf, muf, rsf, logits, loss_rows, lse_rows;
   size_t dres, dbig, dsmall;
   size_t ln_part, ln_part_slab;  // LayerNorm-backward partial rows: 2L+1 slabs of ln_part_slab floats
+  size_t emb_index;              // token index built by the embedding forward, read by its backward
   size_t scalars;  // [loss, norm, coef, pad]
   size_t scratch, scratch_bytes;
   size_t total;
@@ -124,7 +125,7 @@ size_t scratch_need(const bt_gpt2_config& c, int B, int T) {
   mx(bt_attention_bwd_ws_bytes(B, T, c.H, C / c.H));
   mx(bt_layernorm_bwd_ws_bytes(M, C));
   mx(bt_colsum_ws_bytes(M, F > 3 * C ? F : 3 * C));
-  mx(bt_embedding_bwd_ws_bytes(B, T, C, c.Vp));
+  mx(emb_bwd_partials_bytes((long long)M, C));
   mx(bt_grad_norm_ws_bytes(param_offsets(c).total));
   return align_up(s, 256);
 }
@@ -167,6 +168,8 @@ Layout make_layout(const bt_gpt2_config& c, int B, int T) {
   o.ln_part_slab = align_up((size_t)ln_bwd_partial_rows((int)M, (int)C) * 2 * C, 64);
   o.ln_part = take(o.ln_part_slab * (2 * (size_t)c.L + 1));
   o.scalars = take(64);
+  o.emb_index = off;
+  off += align_up(emb_index_bytes((long long)M), 256);
   o.scratch_bytes = scratch_need(c, B, T);
   o.scratch = off;
   off += o.scratch_bytes;
@@ -203,6 +206,11 @@ struct bt_gpt2_ctx {
   size_t ws_bytes;
   int max_B, max_T;
   hipStream_t stream;
+  // the embedding backward's token index is built on a second stream while
+  // the forward runs (fork after the caller's prior work, join before the
+  // embedding backward)
+  hipStream_t side = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_index = nullptr;
   int t;
   ParamOffs po;
   Layout lay;
@@ -355,6 +363,12 @@ extern "C" void bt_gpt2_destroy(bt_gpt2_ctx* ctx) {
     (void)hipStreamSynchronize(ctx->stream);
     for (auto& e : ctx->prof.pool) (void)hipEventDestroy(e);
   }
+  if (ctx->side) {
+    (void)hipStreamSynchronize(ctx->side);
+    (void)hipStreamDestroy(ctx->side);
+  }
+  if (ctx->ev_fork) (void)hipEventDestroy(ctx->ev_fork);
+  if (ctx->ev_index) (void)hipEventDestroy(ctx->ev_index);
   delete ctx;
 }
 
@@ -422,7 +436,23 @@ extern "C" bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, floa
   const double ln_bwd_b0 = f4 * (3 * fM * fC + 2 * fM + 3 * fC);
 
   // ---------------- forward
-  BT_PROF(BT_PROF_EMB_FWD, 0, f4 * (3 * fM * fC), bt_embedding_fwd(tokens, P + po.wte, P + po.wpe, sb.res(0), B, T, C, Vp, s));
+  // token index of the embedding backward, on the side stream (created at
+  // the first step): it waits for everything enqueued so far on the main
+  // stream (the tokens, and any earlier step still reading the index)
+  if (!ctx->side) {
+    BT_CHECK_HIP(hipStreamCreateWithFlags(&ctx->side, hipStreamNonBlocking));
+    BT_CHECK_HIP(hipEventCreateWithFlags(&ctx->ev_fork, hipEventDisableTiming));
+    BT_CHECK_HIP(hipEventCreateWithFlags(&ctx->ev_index, hipEventDisableTiming));
+  }
+  void* emb_index = ctx->ws + ly.emb_index;
+  const size_t emb_index_b = emb_index_bytes((long long)M);
+  BT_CHECK_HIP(hipEventRecord(ctx->ev_fork, s));
+  BT_CHECK_HIP(hipStreamWaitEvent(ctx->side, ctx->ev_fork, 0));
+  BT_TRY(bt_embedding_index(tokens, emb_index, emb_index_b, B, T, Vp, ctx->side));
+  BT_CHECK_HIP(hipEventRecord(ctx->ev_index, ctx->side));
+  // every position reads its wte row, wpe rows once per position t, x0 written
+  BT_PROF(BT_PROF_EMB_FWD, 0, f4 * (2 * fM * fC + (double)T * fC) + 4.0 * fM,
+          bt_embedding_fwd(tokens, P + po.wte, P + po.wpe, sb.res(0), B, T, C, Vp, s));
   for (int l = 0; l < L; ++l) {
     const LayerOffs& w = po.layer[l];
     float* ln1 = sb.layer(ly.ln1, l);
@@ -516,7 +546,12 @@ extern "C" bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, floa
     BT_PROF(BT_PROF_LN_BWD, 0, ln_bwd_b1, ln_bwd(dsm, sb.res(l), P + w.ln1g, sb.layer(ly.mu1, l), sb.layer(ly.rs1, l), 1.f, G + w.ln1g, G + w.ln1b));
   }
   BT_PROF(BT_PROF_LN_BWD, 0, 0, sum_partials_batched(ln_sets.data(), (int)ln_sets.size(), ln_bwd_partial_rows(M, C), 2LL * C, 2 * C, C, beta, s));
-  BT_PROF(BT_PROF_EMB_BWD, 0, f4 * (2 * fM * fC + 2 * (double)T * fC), bt_embedding_bwd(tokens, dres, G + po.wte, G + po.wpe, beta, scr, scrb, B, T, C, Vp, s));
+  // dx0 read once, dwpe written (and read when accumulating); the dwte rows of
+  // the distinct tokens (read + written) depend on the data and are not counted here
+  prof_break(ctx);
+  BT_CHECK_HIP(hipStreamWaitEvent(s, ctx->ev_index, 0));
+  BT_PROF(BT_PROF_EMB_BWD, 0, f4 * (fM * fC + (1.0 + beta) * (double)T * fC),
+          bt_embedding_bwd_indexed(emb_index, emb_index_b, dres, G + po.wte, G + po.wpe, beta, scr, scrb, B, T, C, Vp, s));
   // rows of wpe beyond T receive no gradient in this micro-step
   if (T < cf.max_T && !accumulate) {
     prof_break(ctx);

@@ -221,6 +221,77 @@ def test_embedding(B, T, C, Vp, V):
         assert torch.equal(d2, dwte), "embedding backward not deterministic"
 
 
+def _emb_tokens(kind, B, T, V, Vp):
+    M = B * T
+    if kind == "zipf":
+        return synth.zipf_tokens(M, V, 1.1, 11).reshape(B, T)
+    if kind == "const":        # one run across every piece of the sorted list
+        return np.full((B, T), 3, np.int32)
+    if kind == "blocks64":     # runs of exactly 64 entries: every run boundary on a piece boundary
+        return ((np.arange(M) // 64) % V).astype(np.int32).reshape(B, T)[:, ::-1].copy()
+    if kind == "two_heavy":    # two long runs meeting inside a piece, plus singletons
+        t = np.where(np.arange(M) % 3 == 0, 1, 2).astype(np.int32)
+        t[::97] = np.arange(t[::97].size) % V
+        return t.reshape(B, T)
+    if kind == "clamp":        # ids outside [0, Vp) are clamped to the table
+        t = synth.zipf_tokens(M, V, 1.1, 12)
+        t[::5] = -7
+        t[1::7] = Vp + 3
+        return t.reshape(B, T)
+    raise ValueError(kind)
+
+
+# Backward from a separately built token index (the composed step builds it
+# on a second stream during the forward) against the oracle, and against the
+# self-indexing backward bitwise; forward with clamped ids.
+@pytest.mark.parametrize("B,T,C,Vp,V,kind", [
+    (16, 1024, 768, 50304, 50257, "zipf"),
+    (64, 1024, 64, 50304, 50257, "zipf"),
+    (4, 128, 68, 300, 300, "const"),
+    (2, 512, 12, 64, 64, "blocks64"),
+    (3, 700, 36, 1000, 1000, "two_heavy"),
+    (3, 7, 12, 20, 17, "zipf"),
+    (2, 300, 16, 100, 90, "clamp"),
+    (1, 1, 4, 5, 5, "zipf"),
+    (2, 4096, 20, 70000, 70000, "zipf"),   # 17-bit ids: three digit passes
+])
+def test_embedding_indexed(B, T, C, Vp, V, kind):
+    torch = torch_gpu()
+    say(f"embedding indexed B={B} T={T} C={C} Vp={Vp} {kind}")
+    rng = np.random.Generator(np.random.PCG64(B * 1000 + T))
+    tok = _emb_tokens(kind, B, T, V, Vp)
+    tok_eff = np.clip(tok, 0, Vp - 1)
+    wte = rng.standard_normal((Vp, C)).astype(np.float32)
+    wpe = rng.standard_normal((T, C)).astype(np.float32)
+    tokd = dev(torch, tok)
+    index = torch.empty(bt.lib().bt_embedding_index_bytes(B, T), dtype=torch.uint8, device="cuda")
+    x0 = torch.empty((B * T, C), device="cuda")
+    bt.bt_embedding_fwd(tokd, dev(torch, wte), dev(torch, wpe), x0, B, T, C, Vp)
+    assert np.array_equal(host(x0), ops.embedding_fwd(wte, wpe, tok_eff).reshape(B * T, C).astype(np.float32))
+    bt.bt_embedding_index(tokd, index, B, T, Vp)
+    dx0 = rng.standard_normal((B, T, C)).astype(np.float32)
+    dwte0 = rng.standard_normal((Vp, C)).astype(np.float32)
+    dwpe0 = rng.standard_normal((T, C)).astype(np.float32)
+    rwte, rwpe = ops.embedding_bwd(dx0, tok_eff, Vp, T)
+    dxd = dev(torch, dx0)
+    for beta in (0.0, 1.0):
+        dwte, dwpe = dev(torch, dwte0), dev(torch, dwpe0)
+        bt.bt_embedding_bwd_indexed(index, dxd, dwte, dwpe, beta, B, T, C, Vp)
+        assert_close_maxabs(host(dwte), rwte + dwte0, 1e-5, f"dwte beta={beta}")
+        assert_close_maxabs(host(dwpe), rwpe + beta * dwpe0, 1e-5, f"dwpe beta={beta}")
+        # untouched rows of dwte stay bitwise equal
+        untouched = np.setdiff1d(np.arange(Vp), np.unique(tok_eff))
+        assert np.array_equal(host(dwte)[untouched], dwte0[untouched].astype(np.float64))
+        # the same index again (the arrival counters reset themselves), and the
+        # self-indexing backward: bitwise equal
+        d2, p2 = dev(torch, dwte0), dev(torch, dwpe0)
+        bt.bt_embedding_bwd_indexed(index, dxd, d2, p2, beta, B, T, C, Vp)
+        assert torch.equal(d2, dwte) and torch.equal(p2, dwpe), "indexed backward not deterministic"
+        d3, p3 = dev(torch, dwte0), dev(torch, dwpe0)
+        bt.bt_embedding_bwd(tokd, dxd, d3, p3, beta, B, T, C, Vp)
+        assert torch.equal(d3, dwte) and torch.equal(p3, dwpe), "indexed and self-indexing backward differ"
+
+
 # ---------------------------------------------------------------- Column sums
 @pytest.mark.parametrize("M,N", [(16384, 3072), (37, 20), (1, 4), (16384, 2304)])
 def test_colsum(M, N):
