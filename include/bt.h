@@ -46,12 +46,15 @@ typedef enum {
   BT_EALIGN = 3,      /* pointer or leading dimension not suitably aligned */
   BT_EWORKSPACE = 4,  /* workspace missing or smaller than the query says */
   BT_EHIP = 5,        /* a HIP runtime call or kernel launch failed */
-  BT_ENONFINITE = 6   /* reserved: non-finite value detected on the host */
+  BT_ENONFINITE = 6   /* non-finite gradient norm: the optimizer step was skipped */
 } bt_status;
 
 const char* bt_status_str(bt_status s);
-/* Detail string of the last non-OK status returned on this host thread. */
+/* Detail string and status of the last failure on this host thread.  Every
+ * entry point that returns a bt_status (and bt_gpt2_train_step) clears both
+ * when it starts, so after a successful call they are "" and BT_OK. */
 const char* bt_last_error(void);
+bt_status bt_last_status(void);
 /* Library version, "major.minor.patch". */
 const char* bt_version(void);
 
@@ -281,9 +284,12 @@ bt_status bt_gelu_bwd(const float* x, const float* dy, float* dx, size_t n, void
  * of the forward against the target; appendix "Sparse Cross-Entropy Loss").
  *   lse[m]       = log sum_{j<V} exp(z[m, j])
  *   loss_rows[m] = lse[m] - z[m, targets[m]]
- * targets in [0, V).  Vp multiple of 4, V <= Vp.  Out-of-range targets give
- * BT_EINVAL only if detected on the host; on the device they are clamped and
- * the row's loss is set to NaN.
+ * targets in [0, V).  Vp multiple of 4, V <= Vp.  The targets live on the
+ * device and are not checked on the host: a row whose target lies outside
+ * [0, V) gets a NaN loss and (in the backward and fused calls) a NaN gradient
+ * in its columns < V, so that a training step over it reports a non-finite
+ * gradient norm and skips its update instead of training toward a wrong
+ * class.
  */
 bt_status bt_softmax_xent_fwd(const float* logits, const int32_t* targets, float* loss_rows,
                               float* lse, int M, int V, int Vp, void* stream);
@@ -302,6 +308,8 @@ bt_status bt_softmax_xent_fused(float* logits, const int32_t* targets, float* lo
  * c = *grad_scale (1 if grad_scale is NULL) and d = (i < n_decay):
  *   g = c * g[i];  m = b1 m + (1-b1) g;  v = b2 v + (1-b2) g^2
  *   p = p - lr*wd*d*p - lr * (m / (1-b1^t)) / (sqrt(v / (1-b2^t)) + eps)
+ * If *grad_scale is not finite, nothing is written (p, m, v keep their
+ * values): a non-finite gradient norm skips the step.
  * t >= 1.  n and n_decay multiples of 4, n_decay <= n.  The scalars are
  * host doubles: 1 - beta and the bias corrections are formed in double and
  * rounded to FP32 once (0.999 itself is not an FP32 number; 1 - 0.999f would
@@ -314,8 +322,11 @@ bt_status bt_adamw_step(float* p, const float* g, float* m, float* v, size_t n, 
 /*
  * Global gradient-norm clip (hyper-parameter table: gradient clip 1.0):
  *   norm = sqrt(sum_i g[i]^2);  coef = min(1, clip / (norm + 1e-6))  (coef = 1 if clip <= 0)
- * Writes the two device scalars out_norm[0], out_coef[0].  Fixed-order
- * two-stage reduction.  ws holds bt_grad_norm_ws_bytes(n) bytes.  n multiple of 4.
+ * and coef = NaN whenever norm is not finite (a NaN or Inf gradient), with or
+ * without clipping, so that bt_adamw_step given this coefficient skips the
+ * update.  Writes the two device scalars out_norm[0], out_coef[0].
+ * Fixed-order two-stage reduction.  ws holds bt_grad_norm_ws_bytes(n) bytes.
+ * n multiple of 4.
  */
 bt_status bt_grad_norm_clip(const float* g, size_t n, float clip, float* out_norm,
                             float* out_coef, void* ws, size_t ws_bytes, void* stream);
@@ -386,8 +397,8 @@ typedef struct {
   int Vp;           /* padded rows of wte (multiple of 4) */
   int max_T;        /* rows of wpe */
   int L;            /* layers */
-  int H;            /* heads; C / H must be 64 */
-  int C;            /* model width, multiple of 64 */
+  int H;            /* heads; the head dim C / H a multiple of 4, at most 128 */
+  int C;            /* model width, multiple of 4, at most 4096 */
   float ln_eps;     /* LayerNorm epsilon */
   double lr, beta1, beta2, adam_eps, weight_decay;  /* AdamW (host scalars) */
   double grad_clip; /* <= 0: no clipping */
@@ -427,19 +438,23 @@ void bt_gpt2_set_step_count(bt_gpt2_ctx* ctx, int t);
  * d_loss (device scalar) receives loss_scale * sum of per-position losses,
  * added to its previous value when accumulate = 1.  For one plain step use
  * loss_scale = 1/(B*T); for k micro-steps 1/(B*T*k).  tokens, targets
- * [B, T]; B <= max_B, T <= max_T of the context and T <= cfg.max_T.
+ * [B, T]; B <= max_B, T <= max_T of the context and T <= cfg.max_T, B*T a
+ * multiple of 4 (else BT_ESHAPE before any launch).
  * loss_rows (optional, device [B*T]) receives the unscaled per-position loss.
  */
 bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, float* grads,
                           const int32_t* tokens, const int32_t* targets, int B, int T,
                           float loss_scale, int accumulate, float* d_loss, float* loss_rows);
 /* Global gradient norm, clip (cfg.grad_clip > 0) and AdamW at step t with
- * learning rate lr.  The norm and clip coefficient stay on the device. */
+ * learning rate lr.  The norm and clip coefficient stay on the device; when
+ * the norm is not finite the AdamW launch writes nothing (read the norm with
+ * bt_gpt2_read_scalars to detect it). */
 bt_status bt_gpt2_optimizer_step(bt_gpt2_ctx* ctx, float* params, float* grads, float* opt_state,
                                  int t, double lr);
 /* Waits for the context's stream, then copies to host out[3] the device
  * scalars [last loss written by bt_gpt2_train_step, gradient norm, clip
- * coefficient] of the last step. */
+ * coefficient (1 without clipping, NaN for a non-finite norm)] of the last
+ * step. */
 bt_status bt_gpt2_read_scalars(const bt_gpt2_ctx* ctx, float* out);
 
 /*
@@ -469,8 +484,10 @@ bt_status bt_gpt2_profile_read(bt_gpt2_ctx* ctx, bt_kernel_stat* out, int reset)
 /*
  * One full training step: forward, backward, clip, AdamW (t = previous
  * count + 1, lr = cfg.lr).  Returns the mean loss over the B*T positions at
- * the pre-update parameters; NaN on error (see bt_last_error()).  Blocks
- * until the step has finished.
+ * the pre-update parameters; NaN on error (bt_last_status() and
+ * bt_last_error() say why).  A non-finite gradient norm (NaN or Inf in any
+ * gradient) returns NaN with BT_ENONFINITE: parameters, moments and the step
+ * counter are left unchanged.  Blocks until the step has finished.
  */
 float bt_gpt2_train_step(bt_gpt2_ctx* ctx, float* params, float* grads, float* opt_state,
                          const int32_t* tokens, const int32_t* targets, int B, int T);

@@ -38,6 +38,13 @@ class BTError(RuntimeError):
         self.status = status
 
 
+class BTNonFiniteError(BTError):
+    """A training step met a non-finite gradient norm and skipped its update."""
+
+
+BT_ENONFINITE = 6
+
+
 PROF_CLASSES = ("gemm", "attn_fwd", "attn_bwd", "ln_fwd", "ln_bwd", "xent", "emb_fwd", "emb_bwd",
                 "colsum", "grad_norm", "adamw", "other")
 
@@ -78,6 +85,7 @@ i64 = _c.c_longlong
 _SIGS = {
     "bt_status_str": (_c.c_char_p, [i32]),
     "bt_last_error": (_c.c_char_p, []),
+    "bt_last_status": (i32, []),
     "bt_version": (_c.c_char_p, []),
     "bt_gemm": (i32, [i32, i32, i32, i32, i32, vp, i32, vp, i32, f32, vp, i32, vp, i32, vp, vp, vp, vp, vp, sz, vp]),
     "bt_gemm_ws_bytes": (sz, [i32, i32, i32, i32, i32, i32]),
@@ -430,12 +438,14 @@ class GPT2:
 
     def train_step(self, tokens, targets) -> float:
         B, T = tokens.shape
-        loss = lib().bt_gpt2_train_step(self._ctx, _p(self.params), _p(self.grads), _p(self.opt_state),
-                                        _p(tokens), _p(targets), B, T)
-        if loss != loss:  # NaN: error or a non-finite loss
-            detail = lib().bt_last_error().decode()
-            if detail:
-                raise BTError(-1, "bt_gpt2_train_step", detail)
+        L = lib()
+        loss = L.bt_gpt2_train_step(self._ctx, _p(self.params), _p(self.grads), _p(self.opt_state),
+                                    _p(tokens), _p(targets), B, T)
+        status = L.bt_last_status()
+        if status == BT_ENONFINITE:
+            raise BTNonFiniteError(status, "bt_gpt2_train_step", L.bt_last_error().decode())
+        if status != 0:
+            raise BTError(status, "bt_gpt2_train_step", L.bt_last_error().decode())
         return float(loss)
 
     def fwd_bwd(self, tokens, targets, loss_scale, accumulate, d_loss, loss_rows=None):

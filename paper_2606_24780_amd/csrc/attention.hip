@@ -894,6 +894,7 @@ using namespace bt;
 
 extern "C" bt_status bt_attention_fwd(const float* qkv, float* out, float* lse, int B, int T, int H,
                                       int hd, void* stream) {
+  bt::clear_error();
   BT_TRY(check_attn(qkv, out, B, T, H, hd, "bt_attention_fwd"));
   BT_RETURN_IF(!lse, BT_EINVAL, "bt_attention_fwd: lse is NULL");
   BT_RETURN_IF(!aligned16(qkv) || !aligned16(out), BT_EALIGN, "bt_attention_fwd: qkv/out must be 16-byte aligned");
@@ -922,6 +923,7 @@ extern "C" size_t bt_attention_bwd_ws_bytes(int B, int T, int H, int hd) {
 extern "C" bt_status bt_attention_bwd(const float* dout, const float* qkv, const float* out,
                                       const float* lse, float* dqkv, void* ws, size_t ws_bytes, int B,
                                       int T, int H, int hd, void* stream) {
+  bt::clear_error();
   BT_TRY(check_attn(qkv, dout, B, T, H, hd, "bt_attention_bwd"));
   BT_RETURN_IF(!out || !lse || !dqkv, BT_EINVAL, "bt_attention_bwd: NULL pointer");
   BT_RETURN_IF(!aligned16(qkv) || !aligned16(out) || !aligned16(dout) || !aligned16(dqkv), BT_EALIGN,
@@ -956,6 +958,7 @@ extern "C" bt_status bt_attention_bwd(const float* dout, const float* qkv, const
 // ---------------------------------------------------------------- context parallelism
 
 extern "C" bt_status bt_cp_rank_segments(int T, int W, int rank, int shard, bt_cp_segments* out) {
+  bt::clear_error();
   BT_RETURN_IF(!out, BT_EINVAL, "bt_cp_rank_segments: out is NULL");
   BT_RETURN_IF(W < 1 || rank < 0 || rank >= W || shard < 0 || shard >= W, BT_EINVAL,
                "bt_cp_rank_segments: rank %d / shard %d outside [0, W=%d)", rank, shard, W);
@@ -973,6 +976,7 @@ extern "C" bt_status bt_cp_rank_segments(int T, int W, int rank, int shard, bt_c
 
 extern "C" bt_status bt_cp_shard_tokens(const int32_t* tokens, int32_t* local, int B, int T, int W, int rank,
                                         void* stream) {
+  bt::clear_error();
   bt_cp_segments g;
   BT_TRY(bt_cp_rank_segments(T, W, rank, rank, &g));
   BT_RETURN_IF(B < 1, BT_ESHAPE, "bt_cp_shard_tokens: B=%d", B);
@@ -988,6 +992,7 @@ extern "C" bt_status bt_cp_shard_tokens(const int32_t* tokens, int32_t* local, i
 extern "C" bt_status bt_attention_block_fwd(const float* qkv, const float* kv, long long kv_stride, float* out,
                                             float* lse, int merge, int B, int H, int hd,
                                             const bt_cp_segments* segs, void* stream) {
+  bt::clear_error();
   AttnSegs sg;
   int Tq = 0;
   BT_TRY(make_segs(segs, H, hd, kv, nullptr, kv_stride, &sg, &Tq, "bt_attention_block_fwd"));
@@ -1004,6 +1009,7 @@ extern "C" bt_status bt_attention_block_fwd(const float* qkv, const float* kv, l
 
 extern "C" bt_status bt_attention_lse_merge(float* out, float* lse, const float* block_out, const float* block_lse,
                                             int B, int T, int H, int hd, void* stream) {
+  bt::clear_error();
   BT_RETURN_IF(B < 1 || T < 1 || H < 1 || hd < 4 || (hd & 3), BT_ESHAPE,
                "bt_attention_lse_merge: bad shape B=%d T=%d H=%d hd=%d", B, T, H, hd);
   BT_RETURN_IF(!out || !lse || !block_out || !block_lse, BT_EINVAL, "bt_attention_lse_merge: NULL pointer");
@@ -1019,6 +1025,7 @@ extern "C" bt_status bt_attention_lse_merge(float* out, float* lse, const float*
 
 extern "C" bt_status bt_attention_rowdot(const float* dout, const float* out, float* D, int B, int T, int H, int hd,
                                          void* stream) {
+  bt::clear_error();
   BT_TRY(check_attn(dout, out, B, T, H, hd, "bt_attention_rowdot"));
   BT_RETURN_IF(!D, BT_EINVAL, "bt_attention_rowdot: D is NULL");
   BT_RETURN_IF(!aligned16(dout) || !aligned16(out), BT_EALIGN,
@@ -1048,6 +1055,7 @@ extern "C" bt_status bt_attention_block_bwd(const float* dout, const float* qkv,
                                             const float* lse, const float* D, float* dqkv, float* dkv,
                                             int accumulate, void* ws, size_t ws_bytes, int B, int H, int hd,
                                             const bt_cp_segments* segs, void* stream) {
+  bt::clear_error();
   AttnSegs sg;
   int Tq = 0;
   BT_TRY(make_segs(segs, H, hd, kv, dkv, kv_stride, &sg, &Tq, "bt_attention_block_bwd"));

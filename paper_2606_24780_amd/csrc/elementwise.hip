@@ -79,6 +79,7 @@ __global__ void __launch_bounds__(EW_THREADS) adamw_kernel(floatx4* __restrict__
                                                            size_t n4, size_t nd4, AdamArgs a,
                                                            const float* __restrict__ grad_scale) {
   const float c = grad_scale ? *grad_scale : 1.f;
+  if (!isfinite(c)) return;  // non-finite gradients: the step is skipped, nothing is written
   const size_t stride = (size_t)gridDim.x * blockDim.x;
   size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
   for (; i + (STREAM_U - 1) * stride < n4; i += STREAM_U * stride) {
@@ -173,6 +174,9 @@ __global__ void __launch_bounds__(NF) norm_finish_kernel(const double* __restric
       coef = (double)clip / (norm + 1e-6);
       if (coef > 1.0) coef = 1.0;
     }
+    // a non-finite norm (a NaN or Inf gradient) gives a NaN coefficient,
+    // with or without clipping: the AdamW update then leaves p, m, v as they are
+    if (!isfinite(norm)) coef = NAN;
     if (out_norm) *out_norm = (float)norm;
     if (out_coef) *out_coef = (float)coef;
   }
@@ -319,6 +323,7 @@ bt_status launch_loss_sum(const float* rows, int n, float scale, int accumulate,
 using namespace bt;
 
 extern "C" bt_status bt_gelu_fwd(const float* x, float* y, size_t n, void* stream) {
+  bt::clear_error();
   BT_RETURN_IF(n & 3, BT_ESHAPE, "bt_gelu_fwd: n=%zu must be a multiple of 4", n);
   if (n == 0) return BT_OK;
   BT_RETURN_IF(!x || !y, BT_EINVAL, "bt_gelu_fwd: NULL pointer");
@@ -330,6 +335,7 @@ extern "C" bt_status bt_gelu_fwd(const float* x, float* y, size_t n, void* strea
 }
 
 extern "C" bt_status bt_gelu_bwd(const float* x, const float* dy, float* dx, size_t n, void* stream) {
+  bt::clear_error();
   BT_RETURN_IF(n & 3, BT_ESHAPE, "bt_gelu_bwd: n=%zu must be a multiple of 4", n);
   if (n == 0) return BT_OK;
   BT_RETURN_IF(!x || !dy || !dx, BT_EINVAL, "bt_gelu_bwd: NULL pointer");
@@ -345,6 +351,7 @@ extern "C" bt_status bt_gelu_bwd(const float* x, const float* dy, float* dx, siz
 extern "C" bt_status bt_adamw_step(float* p, const float* g, float* m, float* v, size_t n, size_t n_decay,
                                    double lr, double beta1, double beta2, double eps, double weight_decay, int t,
                                    const float* grad_scale, void* stream) {
+  bt::clear_error();
   BT_RETURN_IF((n & 3) || (n_decay & 3) || n_decay > n, BT_ESHAPE,
                "bt_adamw_step: n=%zu, n_decay=%zu must be multiples of 4 with n_decay <= n", n, n_decay);
   BT_RETURN_IF(t < 1, BT_EINVAL, "bt_adamw_step: step t=%d must be >= 1", t);
@@ -383,6 +390,7 @@ extern "C" size_t bt_grad_norm_ws_bytes(size_t n) {
 
 extern "C" bt_status bt_grad_norm_clip(const float* g, size_t n, float clip, float* out_norm, float* out_coef,
                                        void* ws, size_t ws_bytes, void* stream) {
+  bt::clear_error();
   BT_RETURN_IF(n & 3, BT_ESHAPE, "bt_grad_norm_clip: n=%zu must be a multiple of 4", n);
   BT_RETURN_IF(!out_norm && !out_coef, BT_EINVAL, "bt_grad_norm_clip: no output");
   BT_RETURN_IF(n > 0 && !g, BT_EINVAL, "bt_grad_norm_clip: g is NULL");
@@ -407,6 +415,7 @@ extern "C" size_t bt_colsum_ws_bytes(int M, int N) {
 
 extern "C" bt_status bt_colsum(const float* X, int M, int N, int ldx, float* out, float beta, void* ws,
                                size_t ws_bytes, void* stream) {
+  bt::clear_error();
   BT_RETURN_IF(M < 0 || N < 0 || (N & 3) || ldx < N || (ldx & 3), BT_ESHAPE,
                "bt_colsum: M=%d N=%d ldx=%d (N, ldx multiples of 4, ldx >= N)", M, N, ldx);
   BT_RETURN_IF(beta != 0.f && beta != 1.f, BT_EINVAL, "bt_colsum: beta must be 0 or 1");

@@ -725,6 +725,7 @@ using namespace bt;
 
 extern "C" bt_status bt_embedding_fwd(const int32_t* tokens, const float* wte, const float* wpe, float* x0, int B,
                                       int T, int C, int Vp, void* stream) {
+  bt::clear_error();
   BT_TRY(check_shape(B, T, C, Vp, "bt_embedding_fwd"));
   if (B * T == 0) return BT_OK;
   BT_RETURN_IF(!tokens || !wte || !wpe || !x0, BT_EINVAL, "bt_embedding_fwd: NULL pointer");
@@ -740,6 +741,7 @@ extern "C" size_t bt_embedding_index_bytes(int B, int T) {
 
 extern "C" bt_status bt_embedding_index(const int32_t* tokens, void* index, size_t index_bytes, int B, int T, int Vp,
                                         void* stream) {
+  bt::clear_error();
   BT_TRY(check_shape(B, T, 4, Vp, "bt_embedding_index"));
   if (B * T == 0) return BT_OK;
   BT_RETURN_IF(!tokens || !index, BT_EINVAL, "bt_embedding_index: NULL pointer");
@@ -761,6 +763,7 @@ extern "C" size_t bt_embedding_bwd_indexed_ws_bytes(int B, int T, int C) {
 extern "C" bt_status bt_embedding_bwd_indexed(const void* index, size_t index_bytes, const float* dx0, float* dwte,
                                               float* dwpe, float wpe_beta, void* ws, size_t ws_bytes, int B, int T,
                                               int C, int Vp, void* stream) {
+  bt::clear_error();
   BT_TRY(check_shape(B, T, C, Vp, "bt_embedding_bwd_indexed"));
   BT_RETURN_IF(wpe_beta != 0.f && wpe_beta != 1.f, BT_EINVAL, "bt_embedding_bwd_indexed: wpe_beta must be 0 or 1");
   if (B * T == 0) return BT_OK;
@@ -787,6 +790,7 @@ extern "C" size_t bt_embedding_bwd_ws_bytes(int B, int T, int C, int Vp) {
 extern "C" bt_status bt_embedding_bwd(const int32_t* tokens, const float* dx0, float* dwte, float* dwpe,
                                       float wpe_beta, void* ws, size_t ws_bytes, int B, int T, int C, int Vp,
                                       void* stream) {
+  bt::clear_error();
   BT_TRY(check_shape(B, T, C, Vp, "bt_embedding_bwd"));
   BT_RETURN_IF(wpe_beta != 0.f && wpe_beta != 1.f, BT_EINVAL, "bt_embedding_bwd: wpe_beta must be 0 or 1");
   const int M = B * T;

@@ -913,6 +913,7 @@ extern "C" bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K, const fl
                              const float* bias, bt_epi epi, float* preact_out,
                              const float* gelu_in, const float* residual, float* colsum_B, void* ws,
                              size_t ws_bytes, void* stream) {
+  bt::clear_error();
   BT_RETURN_IF(opA != BT_OP_N && opA != BT_OP_T, BT_EINVAL, "bt_gemm: bad opA %d", (int)opA);
   BT_RETURN_IF(opB != BT_OP_N && opB != BT_OP_T, BT_EINVAL, "bt_gemm: bad opB %d", (int)opB);
   BT_RETURN_IF(epi < BT_EPI_NONE || epi > BT_EPI_DGELU, BT_EINVAL, "bt_gemm: bad epilogue %d", (int)epi);

@@ -282,6 +282,7 @@ struct ProfScope {
   } while (0)
 
 extern "C" bt_status bt_gpt2_profile_enable(bt_gpt2_ctx* ctx, int enable) {
+  bt::clear_error();
   BT_RETURN_IF(!ctx, BT_EINVAL, "bt_gpt2_profile_enable: ctx is NULL");
   if (enable && ctx->prof.pool.empty()) {
     // Timing-only events: without the system-scope fence an event record
@@ -297,6 +298,7 @@ extern "C" bt_status bt_gpt2_profile_enable(bt_gpt2_ctx* ctx, int enable) {
 }
 
 extern "C" bt_status bt_gpt2_profile_read(bt_gpt2_ctx* ctx, bt_kernel_stat* out, int reset) {
+  bt::clear_error();
   BT_RETURN_IF(!ctx || !out, BT_EINVAL, "bt_gpt2_profile_read: NULL pointer");
   BT_CHECK_HIP(hipStreamSynchronize(ctx->stream));
   BT_TRY(prof_flush(ctx));
@@ -317,6 +319,7 @@ extern "C" size_t bt_gpt2_num_decay_params(const bt_gpt2_config* cfg) {
 }
 
 extern "C" bt_status bt_gpt2_param_offsets(const bt_gpt2_config* cfg, size_t* offsets, int* n_tensors) {
+  bt::clear_error();
   BT_TRY(check_config(cfg));
   BT_RETURN_IF(!n_tensors, BT_EINVAL, "bt_gpt2_param_offsets: n_tensors is NULL");
   const ParamOffs po = param_offsets(*cfg);
@@ -333,6 +336,7 @@ extern "C" size_t bt_gpt2_workspace_bytes(const bt_gpt2_config* cfg, int max_B, 
 
 extern "C" bt_status bt_gpt2_create(const bt_gpt2_config* cfg, void* workspace, size_t ws_bytes, int max_B,
                                     int max_T, void* stream, bt_gpt2_ctx** out) {
+  bt::clear_error();
   BT_TRY(check_config(cfg));
   BT_RETURN_IF(!out, BT_EINVAL, "bt_gpt2_create: out is NULL");
   BT_RETURN_IF(max_B < 1 || max_T < 1 || max_T > cfg->max_T, BT_ESHAPE,
@@ -379,6 +383,7 @@ extern "C" void bt_gpt2_set_step_count(bt_gpt2_ctx* ctx, int t) {
 }
 
 extern "C" bt_status bt_gpt2_read_scalars(const bt_gpt2_ctx* ctx, float* out) {
+  bt::clear_error();
   BT_RETURN_IF(!ctx || !out, BT_EINVAL, "bt_gpt2_read_scalars: NULL pointer");
   BT_CHECK_HIP(hipMemcpyAsync(out, ctx->ws + ctx->lay.scalars, 3 * sizeof(float), hipMemcpyDeviceToHost,
                               ctx->stream));
@@ -403,11 +408,14 @@ struct StepBufs {
 extern "C" bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, float* grads, const int32_t* tokens,
                                      const int32_t* targets, int B, int T, float loss_scale, int accumulate,
                                      float* d_loss, float* loss_rows_out) {
+  bt::clear_error();
   BT_RETURN_IF(!ctx || !params || !grads || !tokens || !targets, BT_EINVAL, "bt_gpt2_fwd_bwd: NULL pointer");
   BT_RETURN_IF(B < 1 || T < 1 || B > ctx->max_B || T > ctx->max_T || (long long)B * T > (long long)ctx->max_B * ctx->max_T,
                BT_ESHAPE, "bt_gpt2_fwd_bwd: B=%d T=%d exceed the context's max_B=%d max_T=%d", B, T, ctx->max_B,
                ctx->max_T);
   BT_RETURN_IF(!aligned16(params) || !aligned16(grads), BT_EALIGN, "bt_gpt2_fwd_bwd: params/grads must be 16-byte aligned");
+  BT_RETURN_IF(((long long)B * T) % 4 != 0, BT_ESHAPE, "bt_gpt2_fwd_bwd: B*T=%lld must be a multiple of 4",
+               (long long)B * T);
   const bt_gpt2_config& cf = ctx->cfg;
   const ParamOffs& po = ctx->po;
   const Layout& ly = ctx->lay;
@@ -562,6 +570,7 @@ extern "C" bt_status bt_gpt2_fwd_bwd(bt_gpt2_ctx* ctx, const float* params, floa
 
 extern "C" bt_status bt_gpt2_optimizer_step(bt_gpt2_ctx* ctx, float* params, float* grads, float* opt_state, int t,
                                             double lr) {
+  bt::clear_error();
   BT_RETURN_IF(!ctx || !params || !grads || !opt_state, BT_EINVAL, "bt_gpt2_optimizer_step: NULL pointer");
   BT_RETURN_IF(t < 1, BT_EINVAL, "bt_gpt2_optimizer_step: t=%d must be >= 1", t);
   const bt_gpt2_config& cf = ctx->cfg;
@@ -569,36 +578,43 @@ extern "C" bt_status bt_gpt2_optimizer_step(bt_gpt2_ctx* ctx, float* params, flo
   prof_break(ctx);
   StepBufs sb{ctx};
   float* d_scal = sb.f(ctx->lay.scalars);
-  const float* coef = nullptr;
+  // the coefficient is 1 without clipping and NaN when the norm is not
+  // finite, in which case the AdamW launch writes nothing
   BT_PROF(BT_PROF_GRAD_NORM, 2.0 * P, 4.0 * P,
           bt_grad_norm_clip(grads, P, (float)cf.grad_clip, d_scal + 1, d_scal + 2, sb.scratch(), sb.scratch_bytes(),
                             ctx->stream));
-  if (cf.grad_clip > 0.0) coef = d_scal + 2;
   BT_PROF(BT_PROF_ADAMW, 0, 28.0 * P,
           bt_adamw_step(params, grads, opt_state, opt_state + P, P, ctx->po.n_decay, lr, cf.beta1, cf.beta2,
-                        cf.adam_eps, cf.weight_decay, t, coef, ctx->stream));
+                        cf.adam_eps, cf.weight_decay, t, d_scal + 2, ctx->stream));
   return BT_OK;
 }
 
 extern "C" float bt_gpt2_train_step(bt_gpt2_ctx* ctx, float* params, float* grads, float* opt_state,
                                     const int32_t* tokens, const int32_t* targets, int B, int T) {
+  bt::clear_error();
   if (!ctx) {
     fail(BT_EINVAL, "bt_gpt2_train_step: ctx is NULL");
     return NAN;
   }
   StepBufs sb{ctx};
-  float* d_loss = sb.f(ctx->lay.scalars);
+  float* d_scal = sb.f(ctx->lay.scalars);  // [loss, norm, coef]
   const float scale = 1.0f / (float)((double)B * T);
-  if (bt_gpt2_fwd_bwd(ctx, params, grads, tokens, targets, B, T, scale, 0, d_loss, nullptr) != BT_OK) return NAN;
+  if (bt_gpt2_fwd_bwd(ctx, params, grads, tokens, targets, B, T, scale, 0, d_scal, nullptr) != BT_OK) return NAN;
   if (bt_gpt2_optimizer_step(ctx, params, grads, opt_state, ctx->t + 1, ctx->cfg.lr) != BT_OK) return NAN;
-  ctx->t += 1;
-  float h_loss = NAN;
-  hipError_t e = hipMemcpyAsync(&h_loss, d_loss, sizeof(float), hipMemcpyDeviceToHost, ctx->stream);
+  float h[3] = {NAN, NAN, NAN};
+  hipError_t e = hipMemcpyAsync(h, d_scal, sizeof(h), hipMemcpyDeviceToHost, ctx->stream);
   if (e == hipSuccess) e = hipStreamSynchronize(ctx->stream);
   if (e != hipSuccess) {
     fail(BT_EHIP, "bt_gpt2_train_step: %s", hipGetErrorString(e));
     return NAN;
   }
   if (ctx->prof.on && prof_flush(ctx) != BT_OK) return NAN;
-  return h_loss;
+  if (!std::isfinite(h[1])) {
+    // AdamW wrote nothing; the step counter stays
+    fail(BT_ENONFINITE, "bt_gpt2_train_step: non-finite gradient norm (%g, loss %g); parameters and moments "
+                        "not updated", (double)h[1], (double)h[0]);
+    return NAN;
+  }
+  ctx->t += 1;
+  return h[0];
 }

@@ -283,6 +283,7 @@ using namespace bt;
 
 extern "C" bt_status bt_layernorm_fwd(const float* x, const float* gamma, const float* beta, float* y,
                                       float* mean, float* rstd, int M, int C, float eps, void* stream) {
+  bt::clear_error();
   BT_TRY(ln_check(M, C, "bt_layernorm_fwd"));
   if (M == 0) return BT_OK;
   BT_RETURN_IF(!x || !gamma || !beta || !y || !mean || !rstd, BT_EINVAL, "bt_layernorm_fwd: NULL pointer");
@@ -309,6 +310,7 @@ extern "C" bt_status bt_layernorm_bwd(const float* dy, const float* x, const flo
                                       const float* rstd, float* dx, float* dgamma, float* dbeta,
                                       float dx_beta, float param_beta, void* ws, size_t ws_bytes, int M,
                                       int C, void* stream) {
+  bt::clear_error();
   BT_TRY(ln_check(M, C, "bt_layernorm_bwd"));
   BT_RETURN_IF((dx_beta != 0.f && dx_beta != 1.f) || (param_beta != 0.f && param_beta != 1.f), BT_EINVAL,
                "bt_layernorm_bwd: dx_beta and param_beta must be 0 or 1");

@@ -4,8 +4,10 @@
 namespace bt {
 
 static thread_local char g_err[512] = "";
+static thread_local bt_status g_status = BT_OK;
 
 bt_status fail(bt_status s, const char* fmt, ...) {
+  g_status = s;
   va_list ap;
   va_start(ap, fmt);
   vsnprintf(g_err, sizeof(g_err), fmt, ap);
@@ -13,7 +15,10 @@ bt_status fail(bt_status s, const char* fmt, ...) {
   return s;
 }
 
-void clear_error() { g_err[0] = 0; }
+void clear_error() {
+  g_err[0] = 0;
+  g_status = BT_OK;
+}
 
 bt_status check_launch(const char* what) {
   hipError_t e = hipGetLastError();
@@ -37,5 +42,7 @@ extern "C" const char* bt_status_str(bt_status s) {
 }
 
 extern "C" const char* bt_last_error(void) { return bt::g_err; }
+
+extern "C" bt_status bt_last_status(void) { return bt::g_status; }
 
 extern "C" const char* bt_version(void) { return "0.1.0"; }

@@ -77,7 +77,7 @@ __global__ void __launch_bounds__(XT) xent_row_kernel(float* logits, const int32
     lse_out[row] = lse;
   }
   if (MODE == 1) {
-    const float inv = scale / s;
+    const float inv = bad ? NAN : scale / s;  // an invalid target: NaN gradient row
     floatx4* dr = reinterpret_cast<floatx4*>(dlogits + (long long)row * Vp);
 #pragma unroll
     for (int i = 0; i < NPT; ++i) {
@@ -185,7 +185,7 @@ __global__ void __launch_bounds__(XT) xent_stream_kernel(float* logits, const in
       loss_rows[row] = bad ? NAN : lse - zy;
       lse_out[row] = lse;
     }
-    const float inv = scale / sum;
+    const float inv = bad ? NAN : scale / sum;  // an invalid target: NaN gradient row
     const auto r = rsrc(row);
 #pragma unroll
     for (int i = 0; i < XS_NPT; ++i) {
@@ -209,6 +209,7 @@ __global__ void __launch_bounds__(256) xent_bwd_kernel(const float* logits, cons
   const int V4 = Vp >> 2;
   const float l = lse[row];
   const int y = targets[row];
+  const float sc = (y < 0 || y >= V) ? NAN : scale;  // an invalid target: NaN gradient row
   const floatx4* zr = reinterpret_cast<const floatx4*>(logits + (long long)row * Vp);
   floatx4* dr = reinterpret_cast<floatx4*>(dlogits + (long long)row * Vp);
   for (int c4 = blockIdx.x * blockDim.x + threadIdx.x; c4 < V4; c4 += gridDim.x * blockDim.x) {
@@ -217,7 +218,7 @@ __global__ void __launch_bounds__(256) xent_bwd_kernel(const float* logits, cons
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int c = 4 * c4 + k;
-      o[k] = c < V ? (exp2_hw((z[k] - l) * LOG2E_X) - (c == y ? 1.f : 0.f)) * scale : 0.f;
+      o[k] = c < V ? (exp2_hw((z[k] - l) * LOG2E_X) - (c == y ? 1.f : 0.f)) * sc : 0.f;
     }
     dr[c4] = o;
   }
@@ -266,6 +267,7 @@ using namespace bt;
 
 extern "C" bt_status bt_softmax_xent_fwd(const float* logits, const int32_t* targets, float* loss_rows, float* lse,
                                          int M, int V, int Vp, void* stream) {
+  bt::clear_error();
   BT_TRY(xent_check(logits, targets, M, V, Vp, "bt_softmax_xent_fwd"));
   if (M == 0) return BT_OK;
   BT_RETURN_IF(!loss_rows || !lse, BT_EINVAL, "bt_softmax_xent_fwd: NULL output");
@@ -275,6 +277,7 @@ extern "C" bt_status bt_softmax_xent_fwd(const float* logits, const int32_t* tar
 
 extern "C" bt_status bt_softmax_xent_bwd(const float* logits, const float* lse, const int32_t* targets,
                                          float* dlogits, float scale, int M, int V, int Vp, void* stream) {
+  bt::clear_error();
   BT_TRY(xent_check(logits, targets, M, V, Vp, "bt_softmax_xent_bwd"));
   if (M == 0) return BT_OK;
   BT_RETURN_IF(!lse || !dlogits, BT_EINVAL, "bt_softmax_xent_bwd: NULL pointer");
@@ -289,6 +292,7 @@ extern "C" bt_status bt_softmax_xent_bwd(const float* logits, const float* lse, 
 
 extern "C" bt_status bt_softmax_xent_fused(float* logits, const int32_t* targets, float* loss_rows, float* lse,
                                            float scale, int M, int V, int Vp, void* stream) {
+  bt::clear_error();
   BT_TRY(xent_check(logits, targets, M, V, Vp, "bt_softmax_xent_fused"));
   if (M == 0) return BT_OK;
   BT_RETURN_IF(!loss_rows || !lse, BT_EINVAL, "bt_softmax_xent_fused: NULL output");

@@ -200,4 +200,20 @@ def test_gpt2_context_validation(lib):
     assert lib.bt_gpt2_step_count(ctx) == 0
     # a step larger than the context's token budget is rejected before any launch
     assert lib.bt_gpt2_fwd_bwd(ctx, FAKE, FAKE, FAKE, FAKE, 4, 32, 1.0, 0, None, None) == BT_ESHAPE
+    # B*T not a multiple of 4 (the products need it): rejected before the embedding launches
+    assert lib.bt_gpt2_fwd_bwd(ctx, FAKE, FAKE, FAKE, FAKE, 1, 31, 1.0, 0, None, None) == BT_ESHAPE
+    assert b"multiple of 4" in lib.bt_last_error()
     lib.bt_gpt2_destroy(ctx)
+
+
+def test_last_status_is_cleared_by_each_call(lib):
+    assert lib.bt_gemm(0, 0, 5, 4, 4, FAKE, 4, FAKE, 4, 0.0, FAKE, 4, None, 0, None, None, None, None, None, 0,
+                       None) == BT_ESHAPE
+    assert lib.bt_last_status() == BT_ESHAPE and lib.bt_last_error() != b""
+    # a later call that succeeds without launching anything clears both
+    assert lib.bt_gelu_fwd(FAKE, FAKE, 0, None) == BT_OK
+    assert lib.bt_last_status() == BT_OK and lib.bt_last_error() == b""
+    assert lib.bt_embedding_index(FAKE, FAKE, 0, 2, 8, 100, None) == BT_EWORKSPACE
+    assert lib.bt_last_status() == BT_EWORKSPACE
+    assert lib.bt_embedding_bwd_indexed(FAKE, 1 << 20, FAKE, FAKE, FAKE, 0.5, FAKE, 1 << 20, 2, 8, 16, 100,
+                                        None) == BT_EINVAL
