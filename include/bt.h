@@ -102,6 +102,28 @@ bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K,
 size_t bt_gemm_ws_bytes(bt_op opA, bt_op opB, int M, int N, int K, bt_epi epi);
 
 /*
+ * bt_gemm for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * operation, arguments and results as bt_gemm (bitwise: the same kernels and
+ * split), minus ws/ws_bytes: the split-K partials go to a static device
+ * array of the library, bt_gemm_noalloc_max_ws_bytes() = 64 MiB, held by
+ * every GPU the library runs on until the process ends (its device address
+ * is looked up once per device on the first call there).  A product whose
+ * bt_gemm_ws_bytes() exceeds that returns BT_EWORKSPACE before anything is
+ * launched (at GPT-2 124M, B = 16: every per-layer product fits; the tied
+ * LM head's input and weight gradients do not).  The call allocates nothing.
+ * All calls on one GPU share the one array, which keeps the last call's
+ * partials: calls that overlap on a GPU (several streams or host threads)
+ * race and must be serialised by the caller.
+ */
+bt_status bt_gemm_noalloc(bt_op opA, bt_op opB, int M, int N, int K,
+                          const float* A, int lda, const float* B, int ldb,
+                          float beta, float* C, int ldc,
+                          const float* bias, bt_epi epi, float* preact_out, const float* gelu_in,
+                          const float* residual, float* colsum_B, void* stream);
+size_t bt_gemm_noalloc_max_ws_bytes(void);
+
+/*
  * Causal multi-head self-attention forward (GPT-2 architecture figure:
  * masked multi-head self-attention; appendix "Attention Forward", causal
  * case).  Per batch b and head h: S = Q K^T / sqrt(hd) with key j visible to

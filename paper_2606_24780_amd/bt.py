@@ -89,6 +89,8 @@ _SIGS = {
     "bt_version": (_c.c_char_p, []),
     "bt_gemm": (i32, [i32, i32, i32, i32, i32, vp, i32, vp, i32, f32, vp, i32, vp, i32, vp, vp, vp, vp, vp, sz, vp]),
     "bt_gemm_ws_bytes": (sz, [i32, i32, i32, i32, i32, i32]),
+    "bt_gemm_noalloc": (i32, [i32, i32, i32, i32, i32, vp, i32, vp, i32, f32, vp, i32, vp, i32, vp, vp, vp, vp, vp]),
+    "bt_gemm_noalloc_max_ws_bytes": (sz, []),
     "bt_attention_fwd": (i32, [vp, vp, vp, i32, i32, i32, i32, vp]),
     "bt_attention_bwd": (i32, [vp, vp, vp, vp, vp, vp, sz, i32, i32, i32, i32, vp]),
     "bt_attention_bwd_ws_bytes": (sz, [i32, i32, i32, i32]),
@@ -213,6 +215,15 @@ def bt_gemm(opA, opB, M, N, K, A, lda, B, ldb, beta, C, ldc, bias=None, epi=EPI_
     _check(L.bt_gemm(opA, opB, M, N, K, _p(A), lda, _p(B), ldb, beta, _p(C), ldc, _p(bias), epi,
                      _p(preact_out), _p(gelu_in), _p(residual), _p(colsum_B), _p(w), nbytes,
                      _stream(stream)), "bt_gemm")
+    return C
+
+
+def bt_gemm_noalloc(opA, opB, M, N, K, A, lda, B, ldb, beta, C, ldc, bias=None, epi=EPI_NONE,
+                    preact_out=None, gelu_in=None, residual=None, colsum_B=None, stream=None):
+    """bt_gemm with the library's static split-K scratch: allocates nothing."""
+    _check(lib().bt_gemm_noalloc(opA, opB, M, N, K, _p(A), lda, _p(B), ldb, beta, _p(C), ldc, _p(bias), epi,
+                                 _p(preact_out), _p(gelu_in), _p(residual), _p(colsum_B), _stream(stream)),
+           "bt_gemm_noalloc")
     return C
 
 

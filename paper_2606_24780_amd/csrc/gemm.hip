@@ -42,6 +42,8 @@
 //  * the weight-gradient product can also return the column sums of dY (the
 //    bias gradient) from the B data it already reads, so the bias gradient
 //    costs no extra pass over dY.
+#include <mutex>
+
 #include "bt_internal.h"
 
 namespace bt {
@@ -1000,4 +1002,53 @@ extern "C" bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K, const fl
     BT_TRY(check_launch("splitk_reduce"));
   }
   return BT_OK;
+}
+
+// ---------------------------------------------------------------------------
+// bt_gemm without a caller workspace: the split-K partials live in a static
+// device array of this library (each GPU the library runs on holds its own
+// copy until the process ends).  In host code `gemm_scratch` names a host-side
+// stand-in, not the device memory: the device address is looked up once per
+// device with hipGetSymbolAddress and only that address is passed to kernels.
+namespace {
+
+constexpr size_t GEMM_SCRATCH_BYTES = 64ull << 20;
+__device__ __align__(256) char gemm_scratch[GEMM_SCRATCH_BYTES];
+
+constexpr int MAX_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[MAX_DEVICES] = {};
+
+bt_status scratch_address(void** out) {
+  int dev = 0;
+  BT_CHECK_HIP(hipGetDevice(&dev));
+  BT_RETURN_IF(dev < 0 || dev >= MAX_DEVICES, BT_EINVAL, "bt_gemm_noalloc: device %d out of range", dev);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    BT_CHECK_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(gemm_scratch)));
+    BT_RETURN_IF(!p, BT_EHIP, "bt_gemm_noalloc: no device address for the scratch array");
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return BT_OK;
+}
+
+}  // namespace
+
+extern "C" size_t bt_gemm_noalloc_max_ws_bytes(void) { return GEMM_SCRATCH_BYTES; }
+
+extern "C" bt_status bt_gemm_noalloc(bt_op opA, bt_op opB, int M, int N, int K, const float* A, int lda,
+                                     const float* B, int ldb, float beta, float* C, int ldc, const float* bias,
+                                     bt_epi epi, float* preact_out, const float* gelu_in, const float* residual,
+                                     float* colsum_B, void* stream) {
+  bt::clear_error();
+  const size_t need = bt_gemm_ws_bytes(opA, opB, M, N, K, epi);
+  BT_RETURN_IF(need > GEMM_SCRATCH_BYTES, BT_EWORKSPACE,
+               "bt_gemm_noalloc: M=%d N=%d K=%d needs %zu bytes of split-K scratch; the library's static scratch "
+               "holds %zu (use bt_gemm with a workspace)", M, N, K, need, GEMM_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if (need > 0) BT_TRY(scratch_address(&ws));
+  return bt_gemm(opA, opB, M, N, K, A, lda, B, ldb, beta, C, ldc, bias, epi, preact_out, gelu_in, residual,
+                 colsum_B, ws, need > 0 ? GEMM_SCRATCH_BYTES : 0, stream);
 }
