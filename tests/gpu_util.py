@@ -56,3 +56,19 @@ def assert_close_maxabs(got, ref, tol, what="", scale=None):
 
 def say(msg):
     print(msg, file=sys.stderr, flush=True)
+
+
+def progress(msg):
+    """A progress line of a long test: to stderr, and appended to
+    gpurun_out/test_progress.log at the repository root (pytest holds the
+    test's own output until it ends)."""
+    import os
+    say(msg)
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    d = os.path.join(root, "gpurun_out")
+    try:
+        os.makedirs(d, exist_ok=True)
+        with open(os.path.join(d, "test_progress.log"), "a") as f:
+            f.write(msg + "\n")
+    except OSError:
+        pass

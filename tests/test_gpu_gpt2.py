@@ -25,7 +25,7 @@ from oracle import gpt2 as og
 from oracle import ops
 from paper_2606_24780_amd import bt, synth
 from tests.golden.make_tiny_step import tiny_inputs
-from tests.gpu_util import assert_close_maxabs, dev, host, say, torch_gpu
+from tests.gpu_util import assert_close_maxabs, dev, host, progress, say, torch_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -312,6 +312,55 @@ def test_gpt2_124m_replicated_sequence_full_step():
 
 
 @pytest.mark.timeout(900)
+def test_gpt2_124m_distinct_sequences_full_step():
+    """The benchmark's own batch: 16 different Zipf sequences of 1024 tokens
+    through the full-size step, against the oracle run one sequence at a time
+    and summed (micro-steps of the data-parallel training-step algorithm,
+    each scaled by 1/(B*T)): the loss, every gradient tensor, the gradient
+    norm and clip coefficient, and the clipped AdamW update."""
+    torch = torch_gpu()
+    cfg, params, x, y = _inputs_124m()
+    hp = synth.HP_124M
+    specs = synth.param_specs(cfg)
+    B, T = x.shape
+    assert len({tuple(r) for r in x}) == B, "the batch must hold distinct sequences"
+    progress("gpt2 124M distinct-sequence train step (B=16, T=1024) on the GPU")
+    model, loss = _gpu_step(torch, cfg, hp, params, x, y)
+    g = _unflat(cfg, model.grads)
+    p = _unflat(cfg, model.params)
+    m = _unflat(cfg, model.m)
+    v = _unflat(cfg, model.v)
+    _, norm_gpu, coef_gpu = model.read_scalars()
+    del model
+    torch.cuda.empty_cache()
+    scale = 1.0 / (B * T)
+    grads, loss_or = None, 0.0
+    for b in range(B):
+        lb, _, cache = og.forward(cfg, params, x[b:b + 1], y[b:b + 1])
+        gb = og.backward(cfg, params, cache, scale)
+        del cache
+        loss_or += lb / B
+        if grads is None:
+            grads = gb
+        else:
+            for n in grads:
+                grads[n] += gb[n]
+        progress(f"oracle sequence {b + 1}/{B} done")
+    zeros = {k: np.zeros(s_, dtype=np.float64) for k, s_, _ in specs}
+    p_or, _, _, norm_or, coef_or = og.optimizer_step(params, grads, zeros, zeros, 1, hp, specs)
+    say(f"loss gpu={loss:.8f} oracle={loss_or:.8f}; norm gpu={norm_gpu:.6f} oracle={norm_or:.6f}")
+    assert abs(loss - loss_or) <= LOSS_TOL * abs(loss_or)
+    assert abs(norm_gpu - norm_or) <= 1e-4 * norm_or
+    assert abs(coef_gpu - coef_or) <= 1e-4 * coef_or
+    for name, _, _ in specs:
+        assert_close_maxabs(g[name], grads[name], GRAD_TOL, f"grad {name}")
+    _, coef = _check_update(cfg, hp, specs, params, g, p, m, v, 1, what="124M distinct")
+    assert abs(coef - coef_gpu) <= 1e-6 * coef
+    _check_end_to_end(hp, specs, params, g, grads, p, p_or, coef_gpu, coef_or)
+    progress("gpt2 124M distinct-sequence step checked")
+
+
+@pytest.mark.timeout(900)
 def test_gpt2_124m_b64_equals_4x16_accumulation():
     """Large-batch path: one step at B=64 against 4 micro-steps of 16 rows
     with gradient accumulation (same tokens); gradients to the gradient bar,
@@ -334,7 +383,11 @@ def test_gpt2_124m_b64_equals_4x16_accumulation():
     big.fwd_bwd(dev(torch, x), dev(torch, y), 1.0 / (64 * 1024), 0, d_loss, rows)
     big.optimizer_step(1, hp.lr)
     torch.cuda.synchronize()
-    say(f"peak device memory at B=64: {torch.cuda.max_memory_allocated() / 2**30:.2f} GiB")
+    peak = torch.cuda.max_memory_allocated() / 2**30
+    progress(f"peak device memory at B=64: {peak:.2f} GiB")
+    # the large-batch step fits comfortably in the 288 GB of one MI355X: parameters,
+    # gradients and moments (2 GB) plus about 0.85 GiB of activations per 1024 tokens
+    assert 40.0 < peak < 80.0, peak
     g64 = _unflat(cfg, big.grads)
     p64, m64, v64 = _unflat(cfg, big.params), _unflat(cfg, big.m), _unflat(cfg, big.v)
     rows64 = host(rows).reshape(64, 1024)
