@@ -6,6 +6,10 @@
     python -m paper_2606_24780_amd.profsum ratio PMC_CSV NUM DEN FULL STEPS [--command CMD]
         per-kernel ratio of two counters of one --pmc pass (e.g. matrix-pipe busy
         cycles per GUI cycle, FULL being the value of a pipe busy every cycle).
+    python -m paper_2606_24780_amd.profsum mode BENCH_JSON STATS_CSV [--command CMD ...]
+        one of bench.py's protocol measurements (--sweep gemm, --block,
+        --kernels): its table of medians beside the rocprofv3 kernel statistics
+        of the same command.
     python -m paper_2606_24780_amd.profsum traffic COPY_FETCH COPY_WRITE STEP_FETCH STEP_WRITE STEPS \
         --stats STATS_CSV --json OUT.json --md OUT.md [--command CMD ...]
         HBM bytes per dispatch from the FETCH_SIZE / WRITE_SIZE passes (KiB per
@@ -257,6 +261,40 @@ def ratio_markdown(path, num, den, full, steps, command=None):
     return "\n".join(out) + "\n"
 
 
+def mode_markdown(bench_json, stats_csv, commands=None):
+    """A bench.py protocol measurement (last JSON line of its output) and the
+    rocprofv3 kernel statistics of the same command, as markdown."""
+    lines = [ln for ln in open(bench_json).read().splitlines() if ln.strip().startswith("{")]
+    rec = json.loads(lines[-1])
+    out = [f"Workload: {rec['config']['workload']}.", ""]
+    if commands:
+        out += ["Commands (from the repository root on the GPU box):", "", "```", *commands, "```", ""]
+    pr = rec.get("protocol", {})
+    out += [f"Protocol: {pr.get('warmup')} warm-up runs, {pr.get('timed')} timed runs, {pr.get('statistic')}; "
+            f"{pr.get('flush')}; {pr.get('timer')}.", ""]
+    rows = rec.get("rows")
+    if rows:
+        keys = [k for k in rows[0].keys() if k not in ("split_k_ws_bytes",)]
+        for r in rows[1:]:
+            keys += [k for k in r if k not in keys and k != "split_k_ws_bytes"]
+        out += ["| " + " | ".join(keys) + " |", "|" + "---|" * len(keys)]
+        for r in rows:
+            out.append("| " + " | ".join(str(r.get(k, "")) for k in keys) + " |")
+        out.append("")
+    if rec.get("value") is not None:
+        out += [f"Headline: {rec['metric']}: {rec['value']} {rec['unit']}"
+                + (f"; roofline {rec['roofline']['achieved']} of {rec['roofline']['peak']} {rec['roofline']['unit']} "
+                   f"= {100 * rec['roofline']['frac']:.1f}%" if rec.get("roofline") else "") + ".", ""]
+    st = read_stats(stats_csv)
+    total = sum(r["total_ns"] for r in st)
+    out += ["rocprofv3 kernel statistics of the same command (every dispatch, warm-up runs and the cache-flush "
+            "fills included):", "", "| kernel | calls | avg us | % of GPU time |", "|---|---:|---:|---:|"]
+    for r in sorted(st, key=lambda r: -r["total_ns"]):
+        out.append(f"| `{short_name(r['name'])}` | {r['calls']} | {r['avg_ns'] / 1e3:.1f} | "
+                   f"{100 * r['total_ns'] / total:.1f} |")
+    return "\n".join(out) + "\n"
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -276,6 +314,10 @@ def main():
     t.add_argument("--json", required=True)
     t.add_argument("--md", required=True)
     t.add_argument("--command", action="append")
+    mo = sub.add_parser("mode")
+    mo.add_argument("bench_json")
+    mo.add_argument("stats")
+    mo.add_argument("--command", action="append")
     r = sub.add_parser("ratio")
     r.add_argument("csv")
     r.add_argument("num")
@@ -284,7 +326,9 @@ def main():
     r.add_argument("steps", type=int)
     r.add_argument("--command")
     a = ap.parse_args()
-    if a.cmd == "ratio":
+    if a.cmd == "mode":
+        print(mode_markdown(a.bench_json, a.stats, a.command), end="")
+    elif a.cmd == "ratio":
         print(ratio_markdown(a.csv, a.num, a.den, a.full, a.steps, a.command), end="")
     elif a.cmd == "stats":
         print(stats_markdown(a.csv, a.steps, a.command, M=a.tokens, C=a.d_model, L=a.layers, VP=a.vocab_padded),

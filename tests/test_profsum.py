@@ -59,3 +59,18 @@ def test_stats_and_traffic_parsing(tmp_path):
     text = open(A.md).read()
     # 100 KiB x 2048 B read and 200 KiB x 1024 B written per dispatch
     assert "| `ln_fwd_kernel<3, 2>` | 25 | 0.2 | 0.2 | 0.4 |" in text
+
+
+def test_mode_markdown(tmp_path):
+    bench = tmp_path / "b.json"
+    bench.write_text('{"progress": 1}\n' + json.dumps({
+        "metric": "m", "value": 2.0, "unit": "u", "config": {"workload": "w"},
+        "roofline": {"achieved": 1.0, "peak": 2.0, "unit": "TFLOP/s", "frac": 0.5},
+        "protocol": {"warmup": 25, "timed": 100, "statistic": "median", "flush": "f", "timer": "t"},
+        "rows": [{"kernel": "a", "median_ms": 0.5}, {"kernel": "b", "median_ms": 1.0, "gbs": 3.0}]}) + "\n")
+    stats = tmp_path / "s.csv"
+    stats.write_text('"Name","Calls","TotalDurationNs","AverageNs","Percentage","MinNs","MaxNs","StdDev"\n'
+                     '"k1",2,4000,2000,80,1,1,0\n"k2",1,1000,1000,20,1,1,0\n')
+    md = profsum.mode_markdown(str(bench), str(stats), ["cmd"])
+    assert "| kernel | median_ms | gbs |" in md and "| b | 1.0 | 3.0 |" in md
+    assert "50.0%" in md and "| `k1` | 2 | 2.0 | 80.0 |" in md
