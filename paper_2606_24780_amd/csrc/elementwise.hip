@@ -35,24 +35,54 @@ unsigned norm_blocks(size_t n4) { return ew_blocks(n4, 32); }
 // in the training step AdamW went from 0.66 to 0.59 ms (5.9 TB/s).
 constexpr int STREAM_U = 4;
 
+// GELU forward / backward: one group of STREAM_U float4 per thread (all its
+// loads issued before its stores; no grid-stride loop), non-temporal.
 __global__ void __launch_bounds__(EW_THREADS) gelu_fwd_kernel(const floatx4* __restrict__ x,
                                                               floatx4* __restrict__ y, size_t n4) {
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (size_t)gridDim.x * blockDim.x) {
-    floatx4 v = x[i], o;
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  floatx4 v[STREAM_U];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) o[k] = gelu_f(v[k]);
-    y[i] = o;
+  for (int u = 0; u < STREAM_U; ++u)
+    if (i + u * stride < n4) v[u] = __builtin_nontemporal_load(x + i + u * stride);
+#pragma unroll
+  for (int u = 0; u < STREAM_U; ++u) {
+    if (i + u * stride < n4) {
+      floatx4 o;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) o[k] = gelu_f(v[u][k]);
+      __builtin_nontemporal_store(o, y + i + u * stride);
+    }
   }
 }
 
 __global__ void __launch_bounds__(EW_THREADS) gelu_bwd_kernel(const floatx4* __restrict__ x, const floatx4* dy,
                                                               floatx4* dx, size_t n4) {
-  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += (size_t)gridDim.x * blockDim.x) {
-    floatx4 v = x[i], g = dy[i], o;
+  const size_t stride = (size_t)gridDim.x * blockDim.x;
+  const size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  floatx4 v[STREAM_U], g[STREAM_U];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) o[k] = g[k] * gelu_grad_f(v[k]);
-    dx[i] = o;
+  for (int u = 0; u < STREAM_U; ++u)
+    if (i + u * stride < n4) {
+      v[u] = __builtin_nontemporal_load(x + i + u * stride);
+      g[u] = __builtin_nontemporal_load(dy + i + u * stride);
+    }
+#pragma unroll
+  for (int u = 0; u < STREAM_U; ++u) {
+    if (i + u * stride < n4) {
+      floatx4 o;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) o[k] = g[u][k] * gelu_grad_f(v[u][k]);
+      __builtin_nontemporal_store(o, dx + i + u * stride);
+    }
   }
+}
+
+// Blocks of the single-group streaming kernels.
+unsigned group_blocks(size_t n4) {
+  size_t nb = (n4 + (size_t)EW_THREADS * STREAM_U - 1) / ((size_t)EW_THREADS * STREAM_U);
+  if (nb < 1) nb = 1;
+  return (unsigned)nb;
 }
 
 struct AdamArgs {
@@ -182,27 +212,30 @@ __global__ void __launch_bounds__(NF) norm_finish_kernel(const double* __restric
   }
 }
 
-// Column sums, stage 1: block b sums rows [b*rpb, (b+1)*rpb) of every column.
+// Column sums, stage 1: block (x, y) sums rows [y COLSUM_ROWS, (y + 1)
+// COLSUM_ROWS) of float4 columns [256 x, 256 x + 256): one partial row per
+// row block, loads issued 16 rows at a time.
+constexpr int COLSUM_ROWS = 32;
 __global__ void __launch_bounds__(EW_THREADS) colsum_partial_kernel(const float* __restrict__ X, int M, int N,
-                                                                    long long ldx, int rpb,
-                                                                    float* __restrict__ part) {
-  const int N4 = N >> 2;
-  const int r0 = blockIdx.x * rpb;
-  const int r1 = min(M, r0 + rpb);
-  for (int c = threadIdx.x; c < N4; c += blockDim.x) {
-    floatx4 s = floatx4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll 8
-    for (int r = r0; r < r1; ++r) s += *reinterpret_cast<const floatx4*>(X + (long long)r * ldx + 4 * c);
-    *reinterpret_cast<floatx4*>(part + (long long)blockIdx.x * N + 4 * c) = s;
+                                                                    long long ldx, float* __restrict__ part) {
+  const int c = blockIdx.x * EW_THREADS + threadIdx.x;
+  if (4 * c >= N) return;
+  const int r0 = blockIdx.y * COLSUM_ROWS;
+  const int r1 = min(M, r0 + COLSUM_ROWS);
+  floatx4 s = floatx4{0.f, 0.f, 0.f, 0.f};
+  for (int rb = r0; rb < r1; rb += 16) {
+    floatx4 v[16];
+#pragma unroll
+    for (int u = 0; u < 16; ++u)
+      v[u] = rb + u < r1 ? __builtin_nontemporal_load(reinterpret_cast<const floatx4*>(X + (long long)(rb + u) * ldx) + c)
+                         : floatx4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int u = 0; u < 16; ++u) s += v[u];
   }
+  *reinterpret_cast<floatx4*>(part + (long long)blockIdx.y * N + 4 * c) = s;
 }
 
-int colsum_blocks(int M) {
-  int nb = (M + 31) / 32;
-  if (nb > 512) nb = 512;
-  if (nb < 1) nb = 1;
-  return nb;
-}
+int colsum_blocks(int M) { return M > 0 ? (M + COLSUM_ROWS - 1) / COLSUM_ROWS : 1; }
 
 }  // namespace
 
@@ -329,7 +362,7 @@ extern "C" bt_status bt_gelu_fwd(const float* x, float* y, size_t n, void* strea
   BT_RETURN_IF(!x || !y, BT_EINVAL, "bt_gelu_fwd: NULL pointer");
   BT_RETURN_IF(!aligned16(x) || !aligned16(y), BT_EALIGN, "bt_gelu_fwd: pointers must be 16-byte aligned");
   const size_t n4 = n / 4;
-  hipLaunchKernelGGL(gelu_fwd_kernel, dim3(ew_blocks(n4)), dim3(EW_THREADS), 0, as_stream(stream),
+  hipLaunchKernelGGL(gelu_fwd_kernel, dim3(group_blocks(n4)), dim3(EW_THREADS), 0, as_stream(stream),
                      reinterpret_cast<const floatx4*>(x), reinterpret_cast<floatx4*>(y), n4);
   return check_launch("gelu_fwd_kernel");
 }
@@ -342,7 +375,7 @@ extern "C" bt_status bt_gelu_bwd(const float* x, const float* dy, float* dx, siz
   BT_RETURN_IF(!aligned16(x) || !aligned16(dy) || !aligned16(dx), BT_EALIGN,
                "bt_gelu_bwd: pointers must be 16-byte aligned");
   const size_t n4 = n / 4;
-  hipLaunchKernelGGL(gelu_bwd_kernel, dim3(ew_blocks(n4)), dim3(EW_THREADS), 0, as_stream(stream),
+  hipLaunchKernelGGL(gelu_bwd_kernel, dim3(group_blocks(n4)), dim3(EW_THREADS), 0, as_stream(stream),
                      reinterpret_cast<const floatx4*>(x), reinterpret_cast<const floatx4*>(dy),
                      reinterpret_cast<floatx4*>(dx), n4);
   return check_launch("gelu_bwd_kernel");
@@ -431,9 +464,10 @@ extern "C" bt_status bt_colsum(const float* X, int M, int N, int ldx, float* out
   BT_RETURN_IF(!ws || ws_bytes < need, BT_EWORKSPACE, "bt_colsum: workspace of %zu bytes needed (got %zu)", need,
                ws_bytes);
   const int nb = colsum_blocks(M);
-  const int rpb = (M + nb - 1) / nb;
+  BT_RETURN_IF(nb > 65535, BT_ESHAPE, "bt_colsum: M=%d too large", M);
   float* part = static_cast<float*>(ws);
-  hipLaunchKernelGGL(colsum_partial_kernel, dim3(nb), dim3(EW_THREADS), 0, s, X, M, N, (long long)ldx, rpb, part);
+  hipLaunchKernelGGL(colsum_partial_kernel, dim3((unsigned)((N / 4 + EW_THREADS - 1) / EW_THREADS), (unsigned)nb),
+                     dim3(EW_THREADS), 0, s, X, M, N, (long long)ldx, part);
   BT_TRY(check_launch("colsum_partial_kernel"));
   return sum_partials(part, nb, N, N, out, N, nullptr, beta, s);
 }

@@ -109,6 +109,8 @@ __global__ void __launch_bounds__(XT) xent_row_kernel(float* logits, const int32
 // kernel below, 1.15 ms (5.7 TB/s) for this one.
 constexpr int XS_NPT = 13, XS_PF = 9, XS_NR = XS_NPT - XS_PF;
 
+// GRAD false: the forward alone (loss rows and lse; logits only read).
+template <bool GRAD>
 __global__ void __launch_bounds__(XT) xent_stream_kernel(float* logits, const int32_t* __restrict__ targets,
                                                          float* __restrict__ loss_rows, float* __restrict__ lse_out,
                                                          float scale, int M, int V, int Vp) {
@@ -142,7 +144,10 @@ __global__ void __launch_bounds__(XT) xent_stream_kernel(float* logits, const in
   for (; row < M; row += G) {
     // the prefetch of this row is complete once at most the 13 stores of the
     // previous row are outstanding; then every wave's part is visible
-    asm volatile("s_waitcnt vmcnt(13)" ::: "memory");
+    if (GRAD)
+      asm volatile("s_waitcnt vmcnt(13)" ::: "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
     floatx4 z[XS_NPT];
 #pragma unroll
@@ -185,6 +190,7 @@ __global__ void __launch_bounds__(XT) xent_stream_kernel(float* logits, const in
       loss_rows[row] = bad ? NAN : lse - zy;
       lse_out[row] = lse;
     }
+    if (!GRAD) continue;
     const float inv = bad ? NAN : scale / sum;  // an invalid target: NaN gradient row
     const auto r = rsrc(row);
 #pragma unroll
@@ -201,26 +207,38 @@ __global__ void __launch_bounds__(XT) xent_stream_kernel(float* logits, const in
   }
 }
 
-// Backward from a stored lse: elementwise over the row.
+// Backward from a stored lse, elementwise: each thread one group of XB_U
+// float4 of a row (all loaded before any is written; no grid-stride loop),
+// non-temporal.
+constexpr int XB_U = 8;
 __global__ void __launch_bounds__(256) xent_bwd_kernel(const float* logits, const float* __restrict__ lse,
                                                        const int32_t* __restrict__ targets, float* dlogits,
                                                        float scale, int V, int Vp) {
-  const int row = blockIdx.y;
   const int V4 = Vp >> 2;
-  const float l = lse[row];
+  const int nbx = (V4 + 256 * XB_U - 1) / (256 * XB_U);
+  const int row = blockIdx.x / nbx, bx = blockIdx.x - row * nbx;
+  const float l = lse[row] * LOG2E_X;
   const int y = targets[row];
   const float sc = (y < 0 || y >= V) ? NAN : scale;  // an invalid target: NaN gradient row
   const floatx4* zr = reinterpret_cast<const floatx4*>(logits + (long long)row * Vp);
   floatx4* dr = reinterpret_cast<floatx4*>(dlogits + (long long)row * Vp);
-  for (int c4 = blockIdx.x * blockDim.x + threadIdx.x; c4 < V4; c4 += gridDim.x * blockDim.x) {
-    const floatx4 z = zr[c4];
-    floatx4 o;
+  const int c0 = bx * (256 * XB_U) + threadIdx.x;
+  floatx4 z[XB_U];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int c = 4 * c4 + k;
-      o[k] = c < V ? (exp2_hw((z[k] - l) * LOG2E_X) - (c == y ? 1.f : 0.f)) * sc : 0.f;
+  for (int u = 0; u < XB_U; ++u)
+    if (c0 + 256 * u < V4) z[u] = __builtin_nontemporal_load(zr + c0 + 256 * u);
+#pragma unroll
+  for (int u = 0; u < XB_U; ++u) {
+    const int c4 = c0 + 256 * u;
+    if (c4 < V4) {
+      floatx4 o;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int c = 4 * c4 + k;
+        o[k] = c < V ? (exp2_hw(z[u][k] * LOG2E_X - l) - (c == y ? 1.f : 0.f)) * sc : 0.f;
+      }
+      __builtin_nontemporal_store(o, dr + c4);
     }
-    dr[c4] = o;
   }
 }
 
@@ -271,6 +289,15 @@ extern "C" bt_status bt_softmax_xent_fwd(const float* logits, const int32_t* tar
   BT_TRY(xent_check(logits, targets, M, V, Vp, "bt_softmax_xent_fwd"));
   if (M == 0) return BT_OK;
   BT_RETURN_IF(!loss_rows || !lse, BT_EINVAL, "bt_softmax_xent_fwd: NULL output");
+  const int V4 = Vp / 4;
+  if (V4 > XT * (XS_NPT - 1) && V4 <= XT * XS_NPT) {
+    const int cus = stream_cus();
+    if (cus > 0) {
+      hipLaunchKernelGGL(xent_stream_kernel<false>, dim3(M < cus ? M : cus), dim3(XT), 0, as_stream(stream),
+                         const_cast<float*>(logits), targets, loss_rows, lse, 0.f, M, V, Vp);
+      return check_launch("xent_stream_kernel");
+    }
+  }
   return launch_rows<0>(const_cast<float*>(logits), targets, loss_rows, lse, nullptr, 0.f, M, V, Vp,
                         as_stream(stream));
 }
@@ -283,10 +310,10 @@ extern "C" bt_status bt_softmax_xent_bwd(const float* logits, const float* lse, 
   BT_RETURN_IF(!lse || !dlogits, BT_EINVAL, "bt_softmax_xent_bwd: NULL pointer");
   BT_RETURN_IF(!aligned16(dlogits), BT_EALIGN, "bt_softmax_xent_bwd: dlogits must be 16-byte aligned");
   const int V4 = Vp / 4;
-  int bx = (V4 + 255) / 256;
-  if (bx > 16) bx = 16;
-  hipLaunchKernelGGL(xent_bwd_kernel, dim3(bx, M), dim3(256), 0, as_stream(stream), logits, lse, targets, dlogits,
-                     scale, V, Vp);
+  const long long nb = (long long)((V4 + 256 * XB_U - 1) / (256 * XB_U)) * M;
+  BT_RETURN_IF(nb > 0x7fffffffLL, BT_ESHAPE, "bt_softmax_xent_bwd: M=%d too large", M);
+  hipLaunchKernelGGL(xent_bwd_kernel, dim3((unsigned)nb), dim3(256), 0, as_stream(stream), logits, lse, targets,
+                     dlogits, scale, V, Vp);
   return check_launch("xent_bwd_kernel");
 }
 
@@ -300,8 +327,8 @@ extern "C" bt_status bt_softmax_xent_fused(float* logits, const int32_t* targets
   if (V4 > XT * (XS_NPT - 1) && V4 <= XT * XS_NPT) {
     const int cus = stream_cus();
     if (cus > 0) {
-      hipLaunchKernelGGL(xent_stream_kernel, dim3(M < cus ? M : cus), dim3(XT), 0, as_stream(stream), logits, targets,
-                         loss_rows, lse, scale, M, V, Vp);
+      hipLaunchKernelGGL(xent_stream_kernel<true>, dim3(M < cus ? M : cus), dim3(XT), 0, as_stream(stream), logits,
+                         targets, loss_rows, lse, scale, M, V, Vp);
       return check_launch("xent_stream_kernel");
     }
   }
