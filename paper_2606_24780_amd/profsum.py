@@ -48,6 +48,22 @@ def gemm_products(M=M, C=C, L=L, VP=VP):
     return fwd * L + [(M, VP, C, 0), (M, C, VP, 0), (VP, C, M, 0)] + bwd * L
 
 
+def gemm_layouts(L=L):
+    """Layout (NN forward, NT input gradient, TN weight gradient) of each
+    product of gemm_products(), in the same order."""
+    return ["NN"] * 4 * L + ["NT", "NN", "TN"] + ["TN", "NT"] * 4 * L
+
+
+def gemm_layout_of(name: str):
+    """Layout of a gemm_f32_mfma dispatch from its first two template
+    arguments (K-contiguous A, K-contiguous B); None for other kernels."""
+    n = short_name(name)
+    if not n.startswith("gemm_f32_mfma<"):
+        return None
+    a, b = [x.strip() for x in n[len("gemm_f32_mfma<"):-1].split(",")[:2]]
+    return {("true", "false"): "NN", ("true", "true"): "NT", ("false", "false"): "TN"}.get((a, b), "TT")
+
+
 def gemm_flops_per_step(**dims):
     return sum(2.0 * m * n * k for m, n, k, _ in gemm_products(**dims))
 
@@ -66,6 +82,19 @@ XENT_BYTES = 8.0 * M * VP
 P_124M = 124475904
 ADAMW_BYTES = 28.0 * P_124M
 SUMSQ_BYTES = 4.0 * P_124M
+T_SEQ = 1024
+# embedding forward: token ids, one wte row per token and the T wpe rows read,
+# the M x C sum written
+EMB_FWD_BYTES = 4.0 * (M + 2 * M * C + T_SEQ * C)
+# token index: ids read, one (key, position) pair per token written
+EMB_INDEX_BYTES = 4.0 * (M + 2 * M)
+
+
+def emb_bwd_bytes(distinct: int) -> float:
+    """Embedding backward (both kernels): the index pairs and dx0 read, dwpe
+    written, and the dwte rows of the `distinct` tokens read and written
+    (accumulated onto the LM head's contribution)."""
+    return 4.0 * (2 * M + M * C + T_SEQ * C + 2 * distinct * C)
 
 
 def short_name(name: str) -> str:
@@ -96,6 +125,12 @@ def kernel_class(name: str) -> str:
         return "adamw"
     if n.startswith("sumsq") or n.startswith("norm_finish"):
         return "grad_norm"
+    if n.startswith("emb_fwd"):
+        return "emb_fwd"
+    if n.startswith("emb_index"):
+        return "emb_index"
+    if n.startswith("emb_bwd") or n.startswith("emb_finish"):
+        return "emb_bwd"
     return "other"
 
 
@@ -184,6 +219,32 @@ def traffic(a):
     steps = a.steps
     launches = 147 * steps
     g = by["gemm"]
+    # per layout: product dispatches (split-K reductions listed on their own)
+    lay = defaultdict(lambda: [0, 0.0, 0.0])
+    for (n, v) in fetch:
+        if kernel_class(n) != "gemm":
+            continue
+        k = gemm_layout_of(n) or "splitk_reduce"
+        lay[k][0] += 1
+        lay[k][1] += v * 1024 * fs
+    for (n, v) in write:
+        if kernel_class(n) != "gemm":
+            continue
+        lay[gemm_layout_of(n) or "splitk_reduce"][2] += v * 1024 * ws
+    alg_lay = defaultdict(float)
+    calls_lay = defaultdict(int)
+    for (m, n, k, e), t in zip(gemm_products(), gemm_layouts()):
+        alg_lay[t] += 4.0 * (m * k + k * n + (1 + e) * m * n)
+        calls_lay[t] += 1
+    per_layout = {}
+    for t in ("NN", "NT", "TN"):
+        meas = (lay[t][1] + lay[t][2]) / steps
+        per_layout[t] = {"calls_per_step": calls_lay[t], "dispatches_per_step": lay[t][0] / steps,
+                         "measured_bytes_per_step": round(meas), "algorithmic_bytes_per_step": round(alg_lay[t]),
+                         "measured_over_algorithmic": round(meas / alg_lay[t], 3) if alg_lay[t] else None}
+    rsum = (lay["splitk_reduce"][1] + lay["splitk_reduce"][2]) / steps
+    per_layout["splitk_reduce"] = {"dispatches_per_step": lay["splitk_reduce"][0] / steps,
+                                   "measured_bytes_per_step": round(rsum)}
     alg = gemm_bytes_per_step()
     rec = {
         "kernel": "gemm_f32_mfma (every bt_gemm call of the step, with its split-K reductions; not the batched "
@@ -201,6 +262,7 @@ def traffic(a):
         "traffic_bytes_per_launch": round((g[1] + g[2]) / launches),
         "algorithmic_bytes_per_step": round(alg),
         "algorithmic_bytes_per_launch": round(alg / 147),
+        "per_layout": per_layout,
         "gemm_source_sha256": code_sha256(os.path.join(HERE, "csrc", "gemm.hip")),
         "sha_note": "sha256 of gemm.hip with // comments and blank lines removed (bench.py code_sha256)",
     }
@@ -212,7 +274,8 @@ def traffic(a):
         for r in read_stats(a.stats):
             dur[short_name(r["name"])] = r["avg_ns"]
     alg_per = {"ln_fwd_kernel": LN_FWD_BYTES, "ln_bwd_kernel": LN_BWD_BYTES, "xent_stream_kernel": XENT_BYTES,
-               "adamw_kernel": ADAMW_BYTES, "sumsq_kernel": SUMSQ_BYTES}
+               "adamw_kernel": ADAMW_BYTES, "sumsq_kernel": SUMSQ_BYTES, "emb_fwd_kernel": EMB_FWD_BYTES,
+               "emb_index_kernel": EMB_INDEX_BYTES}
     out = ["HBM-side bytes per dispatch from rocprofv3 `FETCH_SIZE` and `WRITE_SIZE` (separate passes), "
            f"scaled by a plain 1 GiB copy (counter bytes x {fs:.4f} for FETCH_SIZE, x {ws:.4f} for WRITE_SIZE).", ""]
     if a.command:
@@ -229,6 +292,22 @@ def traffic(a):
         out.append(f"| `{k}` | {nd / steps:g} | {fb / nd / 1e6:.1f} | {wb / nd / 1e6:.1f} | {(fb + wb) / nd / 1e6:.1f} | "
                    f"{base_note / 1e6:.1f} | {(fb + wb) / nd / base_note:.3f} | {d / 1e3 if d else float('nan'):.1f} | "
                    f"{gbs:.0f} | {100 * gbs / HBM_PEAK_GBS:.1f} |")
+    if getattr(a, "distinct", 0):
+        # the two embedding-backward kernels share one algorithmic byte count
+        parts = [k for k in per_kernel if k.startswith("emb_bwd_kernel") or k.startswith("emb_finish_kernel")]
+        if parts:
+            nd = per_kernel[parts[0]][0]
+            fb = sum(per_kernel[k][1] for k in parts)
+            wb = sum(per_kernel[k][2] for k in parts)
+            base = emb_bwd_bytes(a.distinct)
+            d = sum(dur.get(k, float("nan")) for k in parts)
+            gbs = base / (d * 1e-9) / 1e9
+            out.append(f"| `{' + '.join(sorted(parts))}` | {nd / steps:g} | {fb / nd / 1e6:.1f} | {wb / nd / 1e6:.1f} | "
+                       f"{(fb + wb) / nd / 1e6:.1f} | {base / 1e6:.1f} | {(fb + wb) / nd / base:.3f} | {d / 1e3:.1f} | "
+                       f"{gbs:.0f} | {100 * gbs / HBM_PEAK_GBS:.1f} |")
+            out += ["", f"Embedding backward bytes count the dwte rows of the {a.distinct} distinct tokens of the "
+                        "batch (read and written) plus the index pairs, dx0 and dwpe; the index kernel runs on a side "
+                        "stream, overlapped with the first layer's forward."]
     out += ["", f"GEMM class: {g[0] / steps:g} dispatches per step (147 bt_gemm calls); "
             f"{(g[1] + g[2]) / launches / 1e6:.1f} MB per call measured against {alg / 147 / 1e6:.1f} MB algorithmic "
             f"({(g[1] + g[2]) / steps / alg:.2f}x)."]
@@ -314,6 +393,8 @@ def main():
     t.add_argument("--json", required=True)
     t.add_argument("--md", required=True)
     t.add_argument("--command", action="append")
+    t.add_argument("--distinct", type=int, default=0,
+                   help="distinct token ids of the profiled batch (embedding-backward bytes)")
     mo = sub.add_parser("mode")
     mo.add_argument("bench_json")
     mo.add_argument("stats")

@@ -59,6 +59,29 @@ def test_stats_and_traffic_parsing(tmp_path):
     text = open(A.md).read()
     # 100 KiB x 2048 B read and 200 KiB x 1024 B written per dispatch
     assert "| `ln_fwd_kernel<3, 2>` | 25 | 0.2 | 0.2 | 0.4 |" in text
+    assert set(rec["per_layout"]) == {"NN", "NT", "TN", "splitk_reduce"}
+
+
+def test_gemm_layouts():
+    lay = profsum.gemm_layouts()
+    prods = profsum.gemm_products()
+    assert len(lay) == len(prods) == 147
+    assert lay.count("NN") == 49 and lay.count("NT") == 49 and lay.count("TN") == 49
+    # the weight-gradient products reduce over the M = 16384 tokens, the others keep M rows
+    for (m, n, k, e), t in zip(prods, lay):
+        assert (k == profsum.M) == (t == "TN")
+    g = "void bt::(anonymous namespace)::gemm_f32_mfma<{}, {}, 0, false, false, 16, 4, 2, 2, 2, 2, true, 0>(x)"
+    assert profsum.gemm_layout_of(g.format("true", "false")) == "NN"
+    assert profsum.gemm_layout_of(g.format("true", "true")) == "NT"
+    assert profsum.gemm_layout_of(g.format("false", "false")) == "TN"
+    assert profsum.gemm_layout_of("void bt::(anonymous namespace)::splitk_reduce<0>(x)") is None
+
+
+def test_embedding_bytes():
+    # ids + index pairs + dx0 + dwpe + 2 x dwte rows of the distinct tokens, float32
+    M, C, T = 16384, 768, 1024
+    assert profsum.emb_bwd_bytes(4132) == 4.0 * (2 * M + M * C + T * C + 2 * 4132 * C)
+    assert profsum.EMB_FWD_BYTES == 4.0 * (M + 2 * M * C + T * C)
 
 
 def test_mode_markdown(tmp_path):
