@@ -108,42 +108,37 @@ __device__ __forceinline__ int seg_suffix_first(int kfirst, int qpos0) {
   return a > 0 ? (a + 31) / 32 : 0;
 }
 
-// Load rows [r0, r0 + 32) of one of Q/K/V/dO-like matrices into an LDS tile
-// [32][LD] (zero-filled beyond T or hd). src points at (b, token 0, head h);
-// `stride` is the token stride.  256 threads, HDP/4 float4 per row.
-template <int HDP, int LD>
-__device__ __forceinline__ void load_rows(floatx4 (&r)[HDP / 32], const float* __restrict__ src,
-                                          long long stride, int r0, int T, int hd, int tid) {
-  constexpr int PER_ROW = HDP / 4;            // float4 per row
+// Rows [r0, r0 + 32) of one of the Q/K/V/dO-like matrices (src points at
+// (b, token 0, head h), `stride` is the token stride) into registers, HDP/4
+// float4 per row over 256 threads, without branches: rows past T and columns
+// past hd read the last valid row / column group instead (always in bounds,
+// T >= 1, hd >= 4), and store_rows_masked zeroes them when the tile goes to
+// an LDS tile [32][LD].  No register is written between issuing the loads
+// and their use, so the only wait for them is the one before the LDS store.
+template <int HDP>
+__device__ __forceinline__ void load_rows_clamped(floatx4 (&r)[HDP / 32], const float* __restrict__ src,
+                                                  long long stride, int r0, int T, int hd, int tid) {
+  constexpr int PER_ROW = HDP / 4;
   constexpr int ROWS_PER_PASS = 256 / PER_ROW;
-  if (r0 + 32 <= T && hd == HDP) {  // whole tile in range (uniform): no per-element checks
-#pragma unroll
-    for (int i = 0; i < HDP / 32; ++i) {
-      const int row = tid / PER_ROW + ROWS_PER_PASS * i;
-      r[i] = *reinterpret_cast<const floatx4*>(src + (long long)(r0 + row) * stride + 4 * (tid % PER_ROW));
-    }
-    return;
-  }
 #pragma unroll
   for (int i = 0; i < HDP / 32; ++i) {
-    const int row = tid / PER_ROW + ROWS_PER_PASS * i;
-    const int d = 4 * (tid % PER_ROW);
-    const int t = r0 + row;
-    if (t < T && d < hd)
-      r[i] = *reinterpret_cast<const floatx4*>(src + (long long)t * stride + d);
-    else
-      r[i] = floatx4{0.f, 0.f, 0.f, 0.f};
+    const int t = min(r0 + tid / PER_ROW + ROWS_PER_PASS * i, T - 1);
+    const int d = min(4 * (tid % PER_ROW), hd - 4);
+    r[i] = *reinterpret_cast<const floatx4*>(src + (long long)t * stride + d);
   }
 }
 
 template <int HDP, int LD>
-__device__ __forceinline__ void store_rows(float* __restrict__ s, const floatx4 (&r)[HDP / 32], int tid) {
+__device__ __forceinline__ void store_rows_masked(float* __restrict__ s, const floatx4 (&r)[HDP / 32], int tid,
+                                                  int r0, int T, int hd) {
   constexpr int PER_ROW = HDP / 4;
   constexpr int ROWS_PER_PASS = 256 / PER_ROW;
 #pragma unroll
   for (int i = 0; i < HDP / 32; ++i) {
     const int row = tid / PER_ROW + ROWS_PER_PASS * i;
-    *reinterpret_cast<floatx4*>(s + row * LD + 4 * (tid % PER_ROW)) = r[i];
+    const int d = 4 * (tid % PER_ROW);
+    const bool ok = r0 + row < T && d < hd;
+    *reinterpret_cast<floatx4*>(s + row * LD + d) = ok ? r[i] : floatx4{0.f, 0.f, 0.f, 0.f};
   }
 }
 
@@ -354,10 +349,10 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const float* __restric
 
   floatx4 rk[HDP / 32], rv[HDP / 32];
   if (nkb > 0) {
-    load_rows<HDP, LDK>(rk, kbase, ks, key_row(0), Tk, sh.hd, tid);
-    load_rows<HDP, LDV>(rv, vbase, ks, key_row(0), Tk, sh.hd, tid);
-    store_rows<HDP, LDK>(smem, rk, tid);
-    store_rows<HDP, LDV>(smem + KSZ, rv, tid);
+    load_rows_clamped<HDP>(rk, kbase, ks, key_row(0), Tk, sh.hd, tid);
+    load_rows_clamped<HDP>(rv, vbase, ks, key_row(0), Tk, sh.hd, tid);
+    store_rows_masked<HDP, LDK>(smem, rk, tid, key_row(0), Tk, sh.hd);
+    store_rows_masked<HDP, LDV>(smem + KSZ, rv, tid, key_row(0), Tk, sh.hd);
   }
   __syncthreads();
 
@@ -365,8 +360,8 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const float* __restric
     const int cur = kb & 1;
     const bool more = kb + 1 < nkb;
     if (more) {
-      load_rows<HDP, LDK>(rk, kbase, ks, key_row(kb + 1), Tk, sh.hd, tid);
-      load_rows<HDP, LDV>(rv, vbase, ks, key_row(kb + 1), Tk, sh.hd, tid);
+      load_rows_clamped<HDP>(rk, kbase, ks, key_row(kb + 1), Tk, sh.hd, tid);
+      load_rows_clamped<HDP>(rv, vbase, ks, key_row(kb + 1), Tk, sh.hd, tid);
     }
     const int kp0 = key_pos(kb);
     if (kp0 <= wpos + 31) {  // some key of the tile visible to this wave
@@ -406,8 +401,8 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const float* __restric
     }
     if (more) {
       float* sN = smem + (cur ^ 1) * (KSZ + VSZ);
-      store_rows<HDP, LDK>(sN, rk, tid);
-      store_rows<HDP, LDV>(sN + KSZ, rv, tid);
+      store_rows_masked<HDP, LDK>(sN, rk, tid, key_row(kb + 1), Tk, sh.hd);
+      store_rows_masked<HDP, LDV>(sN + KSZ, rv, tid, key_row(kb + 1), Tk, sh.hd);
     }
     __syncthreads();
   }
@@ -503,10 +498,10 @@ __global__ void __launch_bounds__(256, HDP > 64 ? 1 : 2) attn_bwd_dq_kernel(
 
   floatx4 rk[HDP / 32], rv[HDP / 32];
   if (nkb > 0) {
-    load_rows<HDP, LDK>(rk, kbase, ks, key_row(0), Tk, sh.hd, tid);
-    load_rows<HDP, LDV>(rv, vbase, ks, key_row(0), Tk, sh.hd, tid);
-    store_rows<HDP, LDK>(smem, rk, tid);
-    store_rows<HDP, LDV>(smem + KSZ, rv, tid);
+    load_rows_clamped<HDP>(rk, kbase, ks, key_row(0), Tk, sh.hd, tid);
+    load_rows_clamped<HDP>(rv, vbase, ks, key_row(0), Tk, sh.hd, tid);
+    store_rows_masked<HDP, LDK>(smem, rk, tid, key_row(0), Tk, sh.hd);
+    store_rows_masked<HDP, LDV>(smem + KSZ, rv, tid, key_row(0), Tk, sh.hd);
   }
   __syncthreads();
 
@@ -514,8 +509,8 @@ __global__ void __launch_bounds__(256, HDP > 64 ? 1 : 2) attn_bwd_dq_kernel(
     const int cur = kb & 1;
     const bool more = kb + 1 < nkb;
     if (more) {
-      load_rows<HDP, LDK>(rk, kbase, ks, key_row(kb + 1), Tk, sh.hd, tid);
-      load_rows<HDP, LDV>(rv, vbase, ks, key_row(kb + 1), Tk, sh.hd, tid);
+      load_rows_clamped<HDP>(rk, kbase, ks, key_row(kb + 1), Tk, sh.hd, tid);
+      load_rows_clamped<HDP>(rv, vbase, ks, key_row(kb + 1), Tk, sh.hd, tid);
     }
     const int kp0 = key_pos(kb);
     if (kp0 <= wpos + 31) {
@@ -543,8 +538,8 @@ __global__ void __launch_bounds__(256, HDP > 64 ? 1 : 2) attn_bwd_dq_kernel(
     }
     if (more) {
       float* sN = smem + (cur ^ 1) * (KSZ + VSZ);
-      store_rows<HDP, LDK>(sN, rk, tid);
-      store_rows<HDP, LDV>(sN + KSZ, rv, tid);
+      store_rows_masked<HDP, LDK>(sN, rk, tid, key_row(kb + 1), Tk, sh.hd);
+      store_rows_masked<HDP, LDV>(sN + KSZ, rv, tid, key_row(kb + 1), Tk, sh.hd);
     }
     __syncthreads();
   }
@@ -664,25 +659,27 @@ __global__ void __launch_bounds__(256, HDP <= 64 ? 2 : 1) attn_bwd_dkv_kernel(
   float rl = 0.f, rd = 0.f;
   auto load_q = [&](int j) {
     const int r0 = q_row(j);
-    load_rows<HDP, LD>(rq, qbase, rs, r0, sh.T, sh.hd, tid);
-    load_rows<HDP, LD>(rdo, dobase, C, r0, sh.T, sh.hd, tid);
+    load_rows_clamped<HDP>(rq, qbase, rs, r0, sh.T, sh.hd, tid);
+    load_rows_clamped<HDP>(rdo, dobase, C, r0, sh.T, sh.hd, tid);
     if (tid < 32) {
-      const int t = r0 + tid;
-      rl = t < sh.T ? lrow[t] * LOG2E : INFINITY;  // rows past T give P = 0
-      rd = t < sh.T ? drow[t] : 0.f;
+      const int t = min(r0 + tid, sh.T - 1);
+      rl = lrow[t];
+      rd = drow[t];
     }
   };
-  auto store_q = [&](float* sb) {
-    store_rows<HDP, LD>(sb, rq, tid);
-    store_rows<HDP, LD>(sb + TSZ, rdo, tid);
+  auto store_q = [&](float* sb, int j) {
+    const int r0 = q_row(j);
+    store_rows_masked<HDP, LD>(sb, rq, tid, r0, sh.T, sh.hd);
+    store_rows_masked<HDP, LD>(sb + TSZ, rdo, tid, r0, sh.T, sh.hd);
     if (tid < 32) {
-      sb[2 * TSZ + tid] = rl;
-      sb[2 * TSZ + 32 + tid] = rd;
+      const bool ok = r0 + tid < sh.T;
+      sb[2 * TSZ + tid] = ok ? rl * LOG2E : INFINITY;  // rows past T give P = 0
+      sb[2 * TSZ + 32 + tid] = ok ? rd : 0.f;
     }
   };
   if (nq > 0) {
     load_q(0);
-    store_q(smem);
+    store_q(smem, 0);
   }
   __syncthreads();
 
@@ -692,12 +689,14 @@ __global__ void __launch_bounds__(256, HDP <= 64 ? 2 : 1) attn_bwd_dkv_kernel(
     if (more) load_q(j + 1);
     const int qv0 = q_row(j);   // first row of the query tile
     const int qp = q_pos(j);    // its first position
-    if (qp + 31 >= kwpos && kw0 < Tk) {  // some query of the tile sees this wave's keys
+    const bool live = qp + 31 >= kwpos && kw0 < Tk;  // some query of the tile sees this wave's keys
+    floatx16 dp;
+    if (live) {
       const float* sQ = smem + cur * BUF;
       const float* sdO = sQ + TSZ;
       const float* sl = sQ + 2 * TSZ;
       const float* sd = sl + 32;
-      floatx16 s, dp;
+      floatx16 s;
       zero16(s);
       zero16(dp);
       mma_rows_by_reg<HDP, LD>(s, sQ, kf, lr, hh);    // S  [q][key]
@@ -719,7 +718,14 @@ __global__ void __launch_bounds__(256, HDP <= 64 ? 2 : 1) attn_bwd_dkv_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) dp[r] = s[r] * (dp[r] - sd[acc_row(r, hh)]);  // dS
       mma_tile_T_by_acc<HDP, LD>(dk, sQ, dp, lr, hh);  // dK^T[d][key] += Q^T dS
-      if (ds_col && ds_lane) {
+    }
+    // The next tile goes to LDS before this tile's dS is stored: loads and
+    // stores retire in order on one counter, so a wait for the next tile's
+    // loads issued after the stores would also wait for the stores to be
+    // written.
+    if (more) store_q(smem + (cur ^ 1) * BUF, j + 1);
+    if (ds_col && ds_lane) {
+      if (live) {
         if (qv0 + 32 <= sh.T) {  // whole query tile in range (uniform)
 #pragma unroll
           for (int r = 0; r < 16; ++r) ds_col[(long long)(qv0 + acc_row(r, hh)) * Tk] = dp[r] * sm_scale;
@@ -730,18 +736,17 @@ __global__ void __launch_bounds__(256, HDP <= 64 ? 2 : 1) attn_bwd_dkv_kernel(
             if (q < sh.T) ds_col[(long long)q * Tk] = dp[r] * sm_scale;
           }
         }
-      }
-    } else if (ds_col && ds_lane && qp < kwpos) {
-      // query tiles of the diagonal 128-row tile that precede this wave's
-      // keys: fully masked, stored as zeros because the dQ product of that
-      // tile sums keys up to the tile's end
+      } else if (qp < kwpos) {
+        // query tiles of the diagonal 128-row tile that precede this wave's
+        // keys: fully masked, stored as zeros because the dQ product of that
+        // tile sums keys up to the tile's end
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int q = qv0 + acc_row(r, hh);
-        if (q < sh.T) ds_col[(long long)q * Tk] = 0.f;
+        for (int r = 0; r < 16; ++r) {
+          const int q = qv0 + acc_row(r, hh);
+          if (q < sh.T) ds_col[(long long)q * Tk] = 0.f;
+        }
       }
     }
-    if (more) store_q(smem + (cur ^ 1) * BUF);
     __syncthreads();
   }
   float* stage = smem + wave * 32 * (HDP + 4);
