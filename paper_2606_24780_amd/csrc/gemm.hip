@@ -18,7 +18,13 @@
 //    no staging VGPRs, no LDS store instructions.  Ragged shapes stage them
 //    global -> VGPR -> LDS with bounds checks.  On MI355X the direct copies
 //    raised the matrix-pipe busy fraction of the NN / TN products by 3-5
-//    points (measured with SQ_VALU_MFMA_BUSY_CYCLES).
+//    points (measured with SQ_VALU_MFMA_BUSY_CYCLES).  Their addresses are
+//    a wave-uniform tile base in SGPRs plus a fixed per-lane 32-bit offset,
+//    and the LDS destinations are scalar too, so the k-loop spends no vector
+//    instruction on them: a vector instruction a wave issues between its
+//    MFMAs delays them (4-8 cycles each on MI355X), and moving the 64-bit
+//    address arithmetic and readfirstlanes to the scalar unit made the
+//    step's products 4-10% faster.
 //  * LDS layouts follow the source layout: K-contiguous rows [rows][BK] with
 //    an XOR swizzle of 16-byte chunks; MN-contiguous rows [BK][128] with the
 //    32-column halves swapped in every other group of 8 k-rows (direct copy)
@@ -111,11 +117,15 @@ __device__ __forceinline__ int kc_swizzle(int row) {
 __device__ __forceinline__ int mn_swizzle(int k) { return ((k >> 3) & 1) << 5; }
 
 
-// Per-lane sources of the NI direct copies (1 KB slices) a wave issues for
-// one R x BK operand tile at k = k0; later tiles add a fixed stride.
+// Per-lane byte offsets of the NI direct copies (1 KB slices) a wave issues
+// for one R x BK operand tile, relative to the tile's first element (row 0,
+// k 0 of the tile): at most R rows (K-contiguous) or BK rows (MN-contiguous)
+// of the operand, so 32 bits suffice for any leading dimension the ABI takes.
+// The tile's base address is wave-uniform and lives in SGPRs; advancing it
+// by a k-tile is one scalar add, and no vector instruction is spent on the
+// copies in the k-loop.
 template <bool KC, int R, int BK, int NI>
-__device__ __forceinline__ void copy_setup(const float* (&g)[NI], const float* __restrict__ X, long long ld,
-                                           int row0, int k0, int wave, int lane) {
+__device__ __forceinline__ void copy_offsets(unsigned (&o)[NI], long long ld, int wave, int lane) {
 #pragma unroll
   for (int j = 0; j < NI; ++j) {
     const int slice = wave * NI + j;
@@ -123,20 +133,22 @@ __device__ __forceinline__ void copy_setup(const float* (&g)[NI], const float* _
       constexpr int TPR = BK / 4, RPS = 64 / TPR;  // rows per 1 KB slice
       const int row = slice * RPS + lane / TPR;
       const int q = (lane % TPR) ^ kc_swizzle<BK>(row);
-      g[j] = X + (long long)(row0 + row) * ld + k0 + 4 * q;
+      o[j] = (unsigned)(((long long)row * ld + 4 * q) * 4);
     } else {
       constexpr int LPK = R / 4, KPS = 64 / LPK;  // lanes per k-row, k-rows per slice
       const int k = slice * KPS + lane / LPK;
       const int col = (4 * (lane % LPK)) ^ mn_swizzle(k);
-      g[j] = X + (long long)(k0 + k) * ld + row0 + col;
+      o[j] = (unsigned)(((long long)k * ld + col) * 4);
     }
   }
 }
 
+// The NI copies of one operand tile: `base` is the tile's first element
+// (wave-uniform), `lds` the LDS byte address of this wave's first slice.
 template <int NI>
-__device__ __forceinline__ void copy_issue(const float* const (&g)[NI], long long adv, float* tile, int wave) {
+__device__ __forceinline__ void copy_issue(const float* base, const unsigned (&o)[NI], unsigned lds) {
 #pragma unroll
-  for (int j = 0; j < NI; ++j) copy16_to_lds(g[j] + adv, tile + (wave * NI + j) * 256);
+  for (int j = 0; j < NI; ++j) copy16_to_lds_sbase(base, o[j], lds + 1024u * j);
 }
 
 // Global -> register staging of one R x BK operand tile (NV float4 per
@@ -444,8 +456,7 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
       for (int r = 0; r < 16; ++r) acc[a][b][r] = 0.f;
 
   floatx4 ra[NVA], rb[NVB];
-  const float* ga[CA];
-  const float* gb[CB];
+  unsigned oa[CA], ob[CB];
   const long long a_unit = A_KC ? 1 : p.lda;  // source advance per unit of k
   const long long b_unit = B_KC ? 1 : p.ldb;
   // Column sums of op(B) (only for MN-contiguous B, i.e. op(B) = B [K][N]),
@@ -458,19 +469,27 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
   floatx4 csf[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) csf[nb] = floatx4{0.f, 0.f, 0.f, 0.f};
+  // direct copies: per-lane offsets, the block's operand bases at kbeg and
+  // the LDS byte addresses of this wave's slices, all but the offsets scalar
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const float* const a_blk = p.A + (A_KC ? (long long)m0 * p.lda + kbeg : (long long)kbeg * p.lda + m0);
+  const float* const b_blk = p.B + (B_KC ? (long long)n0 * p.ldb + kbeg : (long long)kbeg * p.ldb + n0);
+  const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) float*)smem;
+  const unsigned lds_a = lds0 + 1024u * CA * wave_u, lds_b = lds0 + 4u * A_SZ + 1024u * CB * wave_u;
+  constexpr unsigned BUF_BYTES = 4u * (A_SZ + B_SZ);
   if (DTL) {
-    copy_setup<A_KC, BM, BK, CA>(ga, p.A, p.lda, m0, kbeg, wave, lane);
-    copy_setup<B_KC, BN, BK, CB>(gb, p.B, p.ldb, n0, kbeg, wave, lane);
+    copy_offsets<A_KC, BM, BK, CA>(oa, p.lda, wave_u, lane);
+    copy_offsets<B_KC, BN, BK, CB>(ob, p.ldb, wave_u, lane);
   }
   if (nk > 0) {
     if (DTL) {
-      copy_issue<CA>(ga, koff(0) * a_unit, smem, wave);
-      copy_issue<CB>(gb, koff(0) * b_unit, smem + A_SZ, wave);
+      copy_issue<CA>(a_blk + koff(0) * a_unit, oa, lds_a);
+      copy_issue<CB>(b_blk + koff(0) * b_unit, ob, lds_b);
       wait_copies();
     } else {
       load_tile<A_KC, BM, BK, NT>(ra, p.A, p.lda, m0, p.M, kbeg + koff(0), kend, tid);
       load_tile<B_KC, BN, BK, NT>(rb, p.B, p.ldb, n0, p.N, kbeg + koff(0), kend, tid);
-      if (COLSUM)
+      if (COLSUM && tm == 0)
 #pragma unroll
         for (int i = 0; i < NVB; ++i) csum += rb[i];
       store_tile<A_KC, BM, BK, NT>(smem, ra, tid);
@@ -479,15 +498,19 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
   }
   __syncthreads();
 
+  // Column sums are kept by the first tile row of blocks only (tm == 0), and
+  // in the direct-copy path by its first wave row (the waves that combine
+  // them at the end); everyone else skips the adds (a uniform branch).
+  const bool cs_block = COLSUM && tm == 0;
+  const bool cs_wave = cs_block && wm == 0;
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
     const bool more = kt + 1 < nk;
     if (more) {
       if (DTL) {
         // the other buffer was last read before the previous barrier
-        float* sN = smem + (cur ^ 1) * (A_SZ + B_SZ);
-        copy_issue<CA>(ga, koff(kt + 1) * a_unit, sN, wave);
-        copy_issue<CB>(gb, koff(kt + 1) * b_unit, sN + A_SZ, wave);
+        copy_issue<CA>(a_blk + koff(kt + 1) * a_unit, oa, lds_a + (cur ^ 1) * BUF_BYTES);
+        copy_issue<CB>(b_blk + koff(kt + 1) * b_unit, ob, lds_b + (cur ^ 1) * BUF_BYTES);
       } else {
         const int k0 = kbeg + koff(kt + 1);
         load_tile<A_KC, BM, BK, NT>(ra, p.A, p.lda, m0, p.M, k0, kend, tid);
@@ -516,7 +539,7 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
           for (int nb = 0; nb < NB; ++nb)
             acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(fa[mb][q], fb[nb][q], acc[mb][nb],
                                                                0, 0, 0);
-      if (DTL && COLSUM) {
+      if (DTL && COLSUM && cs_wave) {
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) csf[nb] += fb[nb];
       }
@@ -525,7 +548,7 @@ __global__ void __launch_bounds__(64 * WM * WN, OCC) gemm_f32_mfma(const GemmPar
     if (DTL) {
       wait_copies();
     } else if (more) {
-      if (COLSUM)
+      if (COLSUM && cs_block)
 #pragma unroll
         for (int i = 0; i < NVB; ++i) csum += rb[i];
       float* sN = smem + (cur ^ 1) * (A_SZ + B_SZ);
