@@ -618,9 +618,12 @@ __global__ void __launch_bounds__(256, HDP <= 64 ? 2 : 1) attn_bwd_dkv_kernel(
   const int kwpos = kp0 + 32 * wave;
   const int my_kpos = kwpos + lr;
   const float sm_scale = 1.f / sqrtf((float)sh.hd);
-  // dS / sqrt(hd) for the dQ product, [B, H, T, Tk], column my_k of this lane
-  float* ds_col = dS ? dS + (long long)bh * sh.T * Tk + my_k : nullptr;
+  // dS / sqrt(hd) for the dQ product, [B, H, T, Tk]: this (b, h)'s rows, and
+  // the byte offset of this lane's first element in a query tile (row 4 hh,
+  // column my_k); register r of the tile is a scalar offset further.
+  float* const ds_bh = dS ? dS + (long long)bh * sh.T * Tk : nullptr;
   const bool ds_lane = my_k < Tk;
+  const unsigned ds_voff = 4u * (unsigned)(4 * hh * Tk + my_k);
 
   float kf[HDP / 2], vf[HDP / 2];
   load_reg_operand<HDP>(kf, kbase, ks, my_k, Tk, sh.hd, hh, LOG2E * sm_scale);
@@ -724,28 +727,20 @@ __global__ void __launch_bounds__(256, HDP <= 64 ? 2 : 1) attn_bwd_dkv_kernel(
     // loads issued after the stores would also wait for the stores to be
     // written.
     if (more) store_q(smem + (cur ^ 1) * BUF, j + 1);
-    if (ds_col && ds_lane) {
-      if (live) {
-        if (qv0 + 32 <= sh.T) {  // whole query tile in range (uniform)
+    if (ds_bh && ds_lane && (live || qp < kwpos)) {
+      // One buffer resource per query tile, limited to the tile's rows below
+      // T: the stores of rows past T fall outside it and are dropped.  The
+      // tile base and the per-register offsets are scalars, so the 16
+      // stores need no vector address arithmetic.  Query tiles of the
+      // diagonal 128-row tile that precede this wave's keys are fully masked
+      // and stored as zeros, because the dQ product of that tile sums keys
+      // up to the tile's end.
+      const auto rs = __builtin_amdgcn_make_buffer_rsrc(ds_bh + (long long)qv0 * Tk, (short)0,
+                                                        4 * Tk * min(32, sh.T - qv0), 0x00020000);
 #pragma unroll
-          for (int r = 0; r < 16; ++r) ds_col[(long long)(qv0 + acc_row(r, hh)) * Tk] = dp[r] * sm_scale;
-        } else {
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int q = qv0 + acc_row(r, hh);
-            if (q < sh.T) ds_col[(long long)q * Tk] = dp[r] * sm_scale;
-          }
-        }
-      } else if (qp < kwpos) {
-        // query tiles of the diagonal 128-row tile that precede this wave's
-        // keys: fully masked, stored as zeros because the dQ product of that
-        // tile sums keys up to the tile's end
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int q = qv0 + acc_row(r, hh);
-          if (q < sh.T) ds_col[(long long)q * Tk] = 0.f;
-        }
-      }
+      for (int r = 0; r < 16; ++r)
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(unsigned, live ? dp[r] * sm_scale : 0.f), rs,
+                                              ds_voff, 4 * Tk * (8 * (r >> 2) + (r & 3)), 0);
     }
     __syncthreads();
   }
