@@ -149,7 +149,7 @@ def stats_markdown(path, steps, command=None, **dims):
     out = []
     if command:
         out += ["Command (from the repository root on the GPU box):", "", "```", command, "```", ""]
-    out += [f"The profiled process runs {steps} training steps (warm-up + timed); per-step figures divide by "
+    out += [f"The profiled process runs {steps} training steps (warm-up, timed and profiled passes); per-step figures divide by "
             f"{steps}.", "", "| kernel | calls/step | ms/step | avg us | % of GPU time |", "|---|---:|---:|---:|---:|"]
     for r in sorted(rows, key=lambda r: -r["total_ns"]):
         out.append(f"| `{short_name(r['name'])}` | {r['calls'] / steps:.6g} | {r['total_ns'] / steps / 1e6:.3f} | "
