@@ -145,6 +145,13 @@ __device__ __forceinline__ void copy_offsets(unsigned (&o)[NI], long long ld, in
 
 // The NI copies of one operand tile: `base` is the tile's first element
 // (wave-uniform), `lds` the LDS byte address of this wave's first slice.
+// The per-lane copy offsets are 32-bit: a tile spans at most 256 rows (or
+// k-rows) of its operand, so leading dimensions below 2^22 floats keep every
+// offset below 4 GiB.  Wider operands take the staged path (64-bit addresses).
+inline bool copy_offsets_fit(long long lda, long long ldb) {
+  return lda < (1LL << 22) && ldb < (1LL << 22);
+}
+
 template <int NI>
 __device__ __forceinline__ void copy_issue(const float* base, const unsigned (&o)[NI], unsigned lds) {
 #pragma unroll
@@ -843,7 +850,7 @@ static bt_status launch_batched(GemmParams p, hipStream_t stream) {
   p.tiles_n = (p.N + BN - 1) / BN;
   const long long nblocks = (long long)p.tiles_m * p.tiles_n * p.nbatch;
   BT_RETURN_IF(nblocks > 0x7fffffffLL, BT_ESHAPE, "batched product: too many tiles");
-  const bool dtl = p.M % BM == 0 && p.N % BN == 0 && p.K % BK == 0;
+  const bool dtl = p.M % BM == 0 && p.N % BN == 0 && p.K % BK == 0 && copy_offsets_fit(p.lda, p.ldb);
   if (dtl)
     hipLaunchKernelGGL((gemm_f32_mfma<true, false, BT_EPI_NONE, false, false, BK, OCC, WM, WN, MB, NB, true, BMODE>),
                        dim3((unsigned)nblocks), dim3(64 * WM * WN), 0, stream, p);
@@ -1004,7 +1011,7 @@ extern "C" bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K, const fl
   dim3 grid((unsigned)nblocks);
   hipStream_t s = as_stream(stream);
   const int bk = kTileCfgs[cfg.tc].bk;
-  const bool dtl = M % bm == 0 && N % bn == 0 && K % bk == 0;
+  const bool dtl = M % bm == 0 && N % bn == 0 && K % bk == 0 && copy_offsets_fit(lda, ldb);
   if (akc && !bkc) launch_layout<true, false>(p, cfg, epi, split, dtl, grid, s);
   else if (akc && bkc) launch_layout<true, true>(p, cfg, epi, split, dtl, grid, s);
   else if (!akc && !bkc) launch_layout<false, false>(p, cfg, epi, split, dtl, grid, s);

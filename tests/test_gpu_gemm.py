@@ -181,6 +181,35 @@ def test_gemm_full_tiles_match_ragged_path(ta, tb):
     assert_close_maxabs(C_small, ops.gemm(A_s, B_s, bool(ta), bool(tb)), TOL, "full tiles")
 
 
+@pytest.mark.parametrize("wide", ["A", "B"])
+def test_gemm_wide_leading_dimension(wide):
+    """An operand whose leading dimension reaches 2^22 floats (a 4.2M-float
+    row stride) would overflow the 32-bit per-lane offsets of the direct LDS
+    copies, so such a product takes the staged path: the result equals, bit
+    for bit, the same product on compact operands (direct copies; the same
+    terms in the same order) and matches the oracle."""
+    torch = torch_gpu()
+    say(f"gemm wide leading dimension of {wide}")
+    M, N, K = 128, 128, 256
+    wide_ld = (1 << 22) + 4
+    A, B = _operands(M, N, K, 0, 1)  # A [M][K], B [N][K] (NT)
+    Ad, Bd = dev(torch, A), dev(torch, B)
+    C_ref = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    bt.bt_gemm(bt.OP_N, bt.OP_T, M, N, K, Ad, K, Bd, K, 0.0, C_ref, N)
+    rows = M if wide == "A" else N
+    big = torch.zeros((rows, wide_ld), dtype=torch.float32, device="cuda")
+    big[:, :K] = Ad if wide == "A" else Bd
+    C = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    if wide == "A":
+        bt.bt_gemm(bt.OP_N, bt.OP_T, M, N, K, big, wide_ld, Bd, K, 0.0, C, N)
+    else:
+        bt.bt_gemm(bt.OP_N, bt.OP_T, M, N, K, Ad, K, big, wide_ld, 0.0, C, N)
+    torch.cuda.synchronize()
+    del big
+    assert torch.equal(C, C_ref)
+    assert_close_maxabs(host(C), ops.gemm(A, B, False, True), TOL, "wide leading dimension")
+
+
 def test_gemm_deterministic_split():
     torch = torch_gpu()
     say("gemm determinism (split-K)")
