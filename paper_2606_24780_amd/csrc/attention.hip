@@ -288,10 +288,60 @@ __device__ __forceinline__ void store_T_tile_merge(float* __restrict__ stage, fl
   }
 }
 
+// ---------------------------------------------------- direct-to-LDS tiles
+// The forward's key and value tiles at head dim 64 when every key tile is
+// full: unpadded [32][64] tiles copied straight from global memory into LDS
+// (global_load_lds_dwordx4: a wave instruction moves 1 KB = 4 rows, lane i
+// landing at byte 16 i; a tile is 8 such slices, 2 per wave).  No staging
+// registers, no LDS stores, and every address is a scalar tile base plus a
+// per-lane offset fixed for the whole kernel.  The source of each lane is
+// chosen so the tiles are stored swizzled instead of padded:
+//  * keys (read as float4 along d by 32 consecutive rows): the 16-byte chunk
+//    c of row r is stored at chunk c ^ (r & 15), so the 16 rows a quarter
+//    wave reads land on 16 different bank groups;
+//  * values (read as b32 by 32 consecutive columns, the two lane halves 4
+//    rows apart): rows with bit 2 set have their two 32-column halves
+//    swapped, so the two halves of a wave read different banks.
+__device__ __forceinline__ void fwd_copy_offsets(unsigned (&ok)[2], unsigned (&ov)[2], long long ks, int wave,
+                                                 int lane) {
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const int row = 4 * (2 * wave + j) + lane / 16;
+    const int c4 = 4 * (lane % 16);  // LDS column of this lane's 16 bytes
+    ok[j] = (unsigned)((row * ks + 4 * ((c4 / 4) ^ (row & 15))) * 4);
+    ov[j] = (unsigned)((row * ks + (c4 ^ (((row >> 2) & 1) << 5))) * 4);
+  }
+}
+
+// S = (rows of the swizzled key tile) x (register operand), as
+// mma_rows_by_reg<64, ...> on an unpadded tile.
+__device__ __forceinline__ void mma_rows_by_reg_swz(floatx16& acc, const float* __restrict__ s,
+                                                    const float (&f)[32], int lr, int hh) {
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    const floatx4 a = *reinterpret_cast<const floatx4*>(s + lr * 64 + 4 * ((8 * hh + c) ^ (lr & 15)));
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc = mfma32(a[q], f[4 * c + q], acc);
+  }
+}
+
+// out^T += (swizzled value tile)^T x w, as mma_tile_T_by_acc<64, ...>:
+// register st of lane half hh holds row acc_row(st, hh), whose bit 2 is hh.
+__device__ __forceinline__ void mma_tile_T_by_acc_swz(floatx16 (&out)[2], const float* __restrict__ s,
+                                                      const floatx16& w, int lr, int hh) {
+#pragma unroll
+  for (int db = 0; db < 2; ++db)
+#pragma unroll
+    for (int st = 0; st < 16; ++st) {
+      const float a = s[acc_row(st, hh) * 64 + ((32 * db + lr) ^ (hh << 5))];
+      out[db] = mfma32(a, w[st], out[db]);
+    }
+}
+
 // ---------------------------------------------------------------- forward
 // SEG: one rank's share (keys from sg.kv, visibility by segment positions,
 // optional merge into the running out/lse).
-template <int HDP, bool SEG>
+template <int HDP, bool SEG, bool DTL = false>
 __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const float* __restrict__ qkv,
                                                           float* __restrict__ out,
                                                           float* __restrict__ lse, AttnShape sh,
@@ -348,11 +398,29 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const float* __restric
   auto key_pos = [&](int kb) { return SEG ? (kb < n0 ? sg.k_pos[0] + 32 * kb : sg.k_pos[1] + 32 * (kb - n0)) : 32 * kb; };
 
   floatx4 rk[HDP / 32], rv[HDP / 32];
+  // DTL: key and value tiles copied straight into LDS (below)
+  unsigned ok_[2], ov_[2];
+  const unsigned lds0 = (unsigned)(uintptr_t)(__attribute__((address_space(3))) float*)smem;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  if constexpr (DTL) fwd_copy_offsets(ok_, ov_, ks, wave_u, lane);
+  auto issue = [&](int kb, int buf) {
+    const long long r0 = key_row(kb);
+    const unsigned l = lds0 + 4u * buf * (KSZ + VSZ) + 2048u * wave_u;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) copy16_to_lds_sbase(kbase + r0 * ks, ok_[j], l + 1024u * j);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) copy16_to_lds_sbase(vbase + r0 * ks, ov_[j], l + 4u * KSZ + 1024u * j);
+  };
   if (nkb > 0) {
-    load_rows_clamped<HDP>(rk, kbase, ks, key_row(0), Tk, sh.hd, tid);
-    load_rows_clamped<HDP>(rv, vbase, ks, key_row(0), Tk, sh.hd, tid);
-    store_rows_masked<HDP, LDK>(smem, rk, tid, key_row(0), Tk, sh.hd);
-    store_rows_masked<HDP, LDV>(smem + KSZ, rv, tid, key_row(0), Tk, sh.hd);
+    if constexpr (DTL) {
+      issue(0, 0);
+      wait_copies();
+    } else {
+      load_rows_clamped<HDP>(rk, kbase, ks, key_row(0), Tk, sh.hd, tid);
+      load_rows_clamped<HDP>(rv, vbase, ks, key_row(0), Tk, sh.hd, tid);
+      store_rows_masked<HDP, LDK>(smem, rk, tid, key_row(0), Tk, sh.hd);
+      store_rows_masked<HDP, LDV>(smem + KSZ, rv, tid, key_row(0), Tk, sh.hd);
+    }
   }
   __syncthreads();
 
@@ -360,8 +428,12 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const float* __restric
     const int cur = kb & 1;
     const bool more = kb + 1 < nkb;
     if (more) {
-      load_rows_clamped<HDP>(rk, kbase, ks, key_row(kb + 1), Tk, sh.hd, tid);
-      load_rows_clamped<HDP>(rv, vbase, ks, key_row(kb + 1), Tk, sh.hd, tid);
+      if constexpr (DTL) {
+        issue(kb + 1, cur ^ 1);  // the other buffer was last read before the previous barrier
+      } else {
+        load_rows_clamped<HDP>(rk, kbase, ks, key_row(kb + 1), Tk, sh.hd, tid);
+        load_rows_clamped<HDP>(rv, vbase, ks, key_row(kb + 1), Tk, sh.hd, tid);
+      }
     }
     const int kp0 = key_pos(kb);
     if (kp0 <= wpos + 31) {  // some key of the tile visible to this wave
@@ -369,7 +441,10 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const float* __restric
       const float* sV = sK + KSZ;
       floatx16 s;
       zero16(s);
-      mma_rows_by_reg<HDP, LDK>(s, sK, qf, lr, hh);
+      if constexpr (DTL)
+        mma_rows_by_reg_swz(s, sK, qf, lr, hh);
+      else
+        mma_rows_by_reg<HDP, LDK>(s, sK, qf, lr, hh);
       const int kr0 = key_row(kb);
       if ((kp0 + 31 > wpos) || (kr0 + 32 > Tk)) {  // diagonal or ragged tile (uniform)
 #pragma unroll
@@ -397,9 +472,14 @@ __global__ void __launch_bounds__(256, 2) attn_fwd_kernel(const float* __restric
       for (int db = 0; db < HDP / 32; ++db)
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-      mma_tile_T_by_acc<HDP, LDV>(o, sV, s, lr, hh);
+      if constexpr (DTL)
+        mma_tile_T_by_acc_swz(o, sV, s, lr, hh);
+      else
+        mma_tile_T_by_acc<HDP, LDV>(o, sV, s, lr, hh);
     }
-    if (more) {
+    if constexpr (DTL) {
+      wait_copies();
+    } else if (more) {
       float* sN = smem + (cur ^ 1) * (KSZ + VSZ);
       store_rows_masked<HDP, LDK>(sN, rk, tid, key_row(kb + 1), Tk, sh.hd);
       store_rows_masked<HDP, LDV>(sN + KSZ, rv, tid, key_row(kb + 1), Tk, sh.hd);
@@ -768,8 +848,14 @@ void launch_fwd(int hd, dim3 grid, hipStream_t s, const float* qkv, float* out, 
                 const AttnShape& sh, const AttnSegs& sg) {
   if (hd <= 32)
     hipLaunchKernelGGL((attn_fwd_kernel<32, SEG>), grid, dim3(256), 0, s, qkv, out, lse, sh, sg);
-  else if (hd <= 64)
-    hipLaunchKernelGGL((attn_fwd_kernel<64, SEG>), grid, dim3(256), 0, s, qkv, out, lse, sh, sg);
+  else if (hd <= 64) {
+    // direct-to-LDS key / value tiles when every key tile is full and the
+    // per-lane copy offsets (32 rows of the token stride) fit in 32 bits
+    if (!SEG && hd == 64 && sh.T % 32 == 0 && sh.row_stride < (1LL << 24))
+      hipLaunchKernelGGL((attn_fwd_kernel<64, false, true>), grid, dim3(256), 0, s, qkv, out, lse, sh, sg);
+    else
+      hipLaunchKernelGGL((attn_fwd_kernel<64, SEG>), grid, dim3(256), 0, s, qkv, out, lse, sh, sg);
+  }
   else
     hipLaunchKernelGGL((attn_fwd_kernel<128, SEG>), grid, dim3(256), 0, s, qkv, out, lse, sh, sg);
 }
