@@ -29,7 +29,7 @@ import os
 
 # BLAS / OpenMP threads of the float64 oracle (the CPU baseline), fixed before
 # numpy is first imported: the cores this process may run on, capped by a
-# thread limit the environment already sets (a GPU machine's share of its host).
+# thread limit the environment already sets (this process's share of its host).
 _AFFINITY = len(os.sched_getaffinity(0))
 _ENV_CAP = os.environ.get("OMP_NUM_THREADS")
 ORACLE_THREADS = min(_AFFINITY, int(_ENV_CAP)) if (_ENV_CAP or "").isdigit() and int(_ENV_CAP) > 0 else _AFFINITY
@@ -578,8 +578,8 @@ def main():
         calibrate_copy()
         return
     if a.gpus != 1:
-        print(f"bench.py: only --gpus 1 is supported by this build (got {a.gpus}); "
-              "the multi-GPU data-parallel exchange is not implemented", file=sys.stderr)
+        print(f"bench.py: the benchmark runs on one GPU; only --gpus 1 is supported (got {a.gpus}): "
+              "the multi-GPU data-parallel gradient exchange is not implemented", file=sys.stderr)
         sys.exit(2)
     if a.cp:
         bench_cp(a)

@@ -148,7 +148,7 @@ def stats_markdown(path, steps, command=None, **dims):
     total = sum(r["total_ns"] for r in rows)
     out = []
     if command:
-        out += ["Command (from the repository root on the GPU box):", "", "```", command, "```", ""]
+        out += ["Command (run from the repository root):", "", "```", command, "```", ""]
     out += [f"The profiled process runs {steps} training steps (warm-up, timed and profiled passes); per-step figures divide by "
             f"{steps}.", "", "| kernel | calls/step | ms/step | avg us | % of GPU time |", "|---|---:|---:|---:|---:|"]
     for r in sorted(rows, key=lambda r: -r["total_ns"]):
@@ -279,7 +279,7 @@ def traffic(a):
     out = ["HBM-side bytes per dispatch from rocprofv3 `FETCH_SIZE` and `WRITE_SIZE` (separate passes), "
            f"scaled by a plain 1 GiB copy (counter bytes x {fs:.4f} for FETCH_SIZE, x {ws:.4f} for WRITE_SIZE).", ""]
     if a.command:
-        out += ["Commands (from the repository root on the GPU box):", "", "```"] + a.command + ["```", ""]
+        out += ["Commands (run from the repository root):", "", "```"] + a.command + ["```", ""]
     out += ["| kernel | dispatches/step | read MB | written MB | measured MB | algorithmic MB | measured / alg. "
             "| avg us (stats run) | algorithmic GB/s | % of 8 TB/s |", "|---|---:|---:|---:|---:|---:|---:|---:|---:|---:|"]
     for k, (nd, fb, wb) in sorted(per_kernel.items(), key=lambda x: -(x[1][1] + x[1][2])):
@@ -331,7 +331,7 @@ def ratio_markdown(path, num, den, full, steps, command=None):
                 acc[k][2] += float(r["Counter_Value"])
     out = []
     if command:
-        out += ["Command (from the repository root on the GPU box):", "", "```", command, "```", ""]
+        out += ["Command (run from the repository root):", "", "```", command, "```", ""]
     out += [f"| kernel | dispatches/step | {num} / {den} | of {full:g} |", "|---|---:|---:|---:|"]
     for k, (n, a, b) in sorted(acc.items(), key=lambda x: -x[1][2]):
         if b <= 0 or n == 0 or a <= 0:
@@ -347,7 +347,7 @@ def mode_markdown(bench_json, stats_csv, commands=None):
     rec = json.loads(lines[-1])
     out = [f"Workload: {rec['config']['workload']}.", ""]
     if commands:
-        out += ["Commands (from the repository root on the GPU box):", "", "```", *commands, "```", ""]
+        out += ["Commands (run from the repository root):", "", "```", *commands, "```", ""]
     pr = rec.get("protocol", {})
     out += [f"Protocol: {pr.get('warmup')} warm-up runs, {pr.get('timed')} timed runs, {pr.get('statistic')}; "
             f"{pr.get('flush')}; {pr.get('timer')}.", ""]

@@ -59,16 +59,17 @@ def say(msg):
 
 
 def progress(msg):
-    """A progress line of a long test: to stderr, and appended to
-    gpurun_out/test_progress.log at the repository root (pytest holds the
-    test's own output until it ends)."""
+    """A progress line of a long test: to stderr, and appended to the file
+    named by BT_PROGRESS_LOG when it is set (pytest holds the test's own
+    output until it ends, so a file shows how far a long run got)."""
     import os
     say(msg)
-    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-    d = os.path.join(root, "gpurun_out")
+    path = os.environ.get("BT_PROGRESS_LOG")
+    if not path:
+        return
     try:
-        os.makedirs(d, exist_ok=True)
-        with open(os.path.join(d, "test_progress.log"), "a") as f:
+        os.makedirs(os.path.dirname(os.path.abspath(path)), exist_ok=True)
+        with open(path, "a") as f:
             f.write(msg + "\n")
     except OSError:
         pass
