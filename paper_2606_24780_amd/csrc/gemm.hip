@@ -10,8 +10,10 @@
 //  * block tile 128 x 128 x BK (BK = 16 at 4 blocks per CU, or BK = 32 at 2),
 //    256 threads = 4 waves in a 2 x 2 grid, each wave owns a 64 x 64 sub-tile
 //    = 2 x 2 MFMA 32x32 accumulators (64 VGPRs).  The kernel is written for
-//    any WM x WN wave grid; 256 x 128, 128 x 256 and 256 x 256 block tiles were
-//    measured no faster on the model's shapes and are not launched.
+//    any WM x WN wave grid; 256 x 128, 128 x 256 and 256 x 256 block tiles are
+//    not launched: on MI355X they gain up to 6% on plain products with
+//    thousands of tiles but lose 10-35% on the 768-column products and the
+//    epilogue products, so the model's step is slower with them.
 //  * when every tile of a launch is full (M, N multiples of 128, K range a
 //    multiple of BK: all GPT-2 shapes) operand tiles go straight from global
 //    memory into LDS (global_load_lds_dwordx4, 1 KB per wave instruction):
