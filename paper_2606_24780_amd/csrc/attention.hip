@@ -17,7 +17,10 @@
 //  * a block = 4 waves = 128 query rows (forward, dQ) or 128 key rows (dK/dV);
 //    each wave owns 32 rows and keeps its row operand (Q, or K and V) in
 //    registers; the streamed operand tiles of 32 rows are double-buffered in
-//    LDS and shared by the 4 waves.
+//    LDS and shared by the 4 waves.  The forward at head dim 64 with full key
+//    tiles copies its key and value tiles straight into swizzled LDS tiles
+//    (global_load_lds_dwordx4, scalar tile base); elsewhere tiles are staged
+//    through registers into padded LDS tiles.
 //  * products are computed transposed where that makes the next product's
 //    operand a register the lane already holds: S^T = K Q^T leaves each lane
 //    with one query's 16 scores, so the softmax row statistics are in-lane plus
