@@ -215,7 +215,7 @@ __global__ void __launch_bounds__(NF) norm_finish_kernel(const double* __restric
 // Column sums, stage 1: block (x, y) sums rows [y COLSUM_ROWS, (y + 1)
 // COLSUM_ROWS) of float4 columns [256 x, 256 x + 256): one partial row per
 // row block, loads issued 16 rows at a time.
-constexpr int COLSUM_ROWS = 32;
+constexpr int COLSUM_ROWS = 64;
 __global__ void __launch_bounds__(EW_THREADS) colsum_partial_kernel(const float* __restrict__ X, int M, int N,
                                                                     long long ldx, float* __restrict__ part) {
   const int c = blockIdx.x * EW_THREADS + threadIdx.x;
