@@ -46,11 +46,7 @@ constexpr int PIECE = 32;        // entries of the sorted list per token unit
 constexpr int TV = 1;            // floats per lane in token and finish units
 constexpr int WPE_T = 2;         // positions per position unit
 constexpr int TOK_WAVES = 12;    // column slices (waves) per token-unit workgroup
-// rows per wave in the gather: four rows of up to 768 floats, fewer for wider rows
-template <int NV>
-struct FwdRows {
-  static constexpr int value = NV <= 3 ? 4 : (NV <= 6 ? 2 : 1);
-};
+constexpr int FWD_WAVES = 4;     // rows (one per wave) per gather workgroup
 
 __host__ __device__ int bits_for(long long n) {
   int b = 0;
@@ -439,48 +435,38 @@ __global__ void __launch_bounds__(SORT_THREADS) emb_index_kernel(const int32_t* 
   build_index(tok, M, Vp, ix, sm);
 }
 
-// Forward gather: a wave takes FwdRows<NV> consecutive rows, a lane NV float4
-// columns of each; all rows' wte and wpe loads are issued before the adds.
-// The token id is wave-uniform (a scalar load per row).
+// Forward gather: one wave per row, a lane NV float4 columns of it; the wte
+// and wpe loads are all issued before the adds.  The token id is wave-uniform
+// (one scalar load).  One row per wave measured 8% faster than four (19.6 vs
+// 21.4 us at 16384 x 768 inside the step): more, shorter waves overlap the
+// dependent token-id load and the stores better.
 template <int NV>
-__global__ void __launch_bounds__(256) emb_fwd_kernel(const int32_t* __restrict__ tok,
-                                                      const float* __restrict__ wte,
-                                                      const float* __restrict__ wpe, float* __restrict__ x0, int M,
-                                                      int T, int C, int Vp) {
-  constexpr int FWD_ROWS = FwdRows<NV>::value;
+__global__ void __launch_bounds__(64 * FWD_WAVES) emb_fwd_kernel(const int32_t* __restrict__ tok,
+                                                                 const float* __restrict__ wte,
+                                                                 const float* __restrict__ wpe,
+                                                                 float* __restrict__ x0, int M, int T, int C,
+                                                                 int Vp) {
   const int lane = threadIdx.x & 63;
-  const int m0 = (blockIdx.x * 4 + (threadIdx.x >> 6)) * FWD_ROWS;
-  if (m0 >= M) return;
+  const int m = blockIdx.x * FWD_WAVES + (threadIdx.x >> 6);
+  if (m >= M) return;
   const int C4 = C >> 2;
-  floatx4 a[FWD_ROWS][NV], b[FWD_ROWS][NV];
+  const int id = clamp_tok(__builtin_amdgcn_readfirstlane(tok[m]), Vp);
+  const floatx4* wr = reinterpret_cast<const floatx4*>(wte + (long long)id * C);
+  const floatx4* pr = reinterpret_cast<const floatx4*>(wpe + (long long)(m % T) * C);
+  floatx4 a[NV], b[NV];
 #pragma unroll
-  for (int r = 0; r < FWD_ROWS; ++r) {
-    const int m = m0 + r;
-    if (m < M) {
-      const int id = clamp_tok(__builtin_amdgcn_readfirstlane(tok[m]), Vp);
-      const floatx4* wr = reinterpret_cast<const floatx4*>(wte + (long long)id * C);
-      const floatx4* pr = reinterpret_cast<const floatx4*>(wpe + (long long)(m % T) * C);
-#pragma unroll
-      for (int i = 0; i < NV; ++i) {
-        const int c = lane + 64 * i;
-        if (c < C4) {
-          a[r][i] = wr[c];
-          b[r][i] = pr[c];
-        }
-      }
+  for (int i = 0; i < NV; ++i) {
+    const int c = lane + 64 * i;
+    if (c < C4) {
+      a[i] = wr[c];
+      b[i] = pr[c];
     }
   }
+  floatx4* xr = reinterpret_cast<floatx4*>(x0 + (long long)m * C);
 #pragma unroll
-  for (int r = 0; r < FWD_ROWS; ++r) {
-    const int m = m0 + r;
-    if (m < M) {
-      floatx4* xr = reinterpret_cast<floatx4*>(x0 + (long long)m * C);
-#pragma unroll
-      for (int i = 0; i < NV; ++i) {
-        const int c = lane + 64 * i;
-        if (c < C4) xr[c] = a[r][i] + b[r][i];
-      }
-    }
+  for (int i = 0; i < NV; ++i) {
+    const int c = lane + 64 * i;
+    if (c < C4) xr[c] = a[i] + b[i];
   }
 }
 
@@ -670,8 +656,8 @@ bt_status launch_fwd(const int32_t* tokens, const float* wte, const float* wpe, 
   const int M = B * T;
   const int nv = (C / 4 + 63) / 64;
 #define BT_EMB_FWD(NV)                                                                                   \
-  hipLaunchKernelGGL(emb_fwd_kernel<NV>, dim3((unsigned)((M + 4 * FwdRows<NV>::value - 1) / (4 * FwdRows<NV>::value))), \
-                     dim3(256), 0, s, tokens, wte, wpe, x0, M, T, C, Vp)
+  hipLaunchKernelGGL(emb_fwd_kernel<NV>, dim3((unsigned)((M + FWD_WAVES - 1) / FWD_WAVES)), dim3(64 * FWD_WAVES), \
+                     0, s, tokens, wte, wpe, x0, M, T, C, Vp)
   switch (nv) {
     case 1: BT_EMB_FWD(1); break;
     case 2: BT_EMB_FWD(2); break;
