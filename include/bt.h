@@ -269,7 +269,7 @@ size_t bt_attention_block_bwd_ws_bytes(int B, int H, int hd, const bt_cp_segment
  *   mean = sum_c x / C, var = sum_c (x - mean)^2 / C, rstd = 1/sqrt(var + eps)
  *   y = gamma * (x - mean) * rstd + beta
  * x, y [M, C]; mean, rstd [M] (written, for the backward).  C multiple of 4,
- * C <= 4096.  y must not alias x.
+ * C <= 4096, M >= 0 (M = 0 writes nothing).  y must not alias x.
  */
 bt_status bt_layernorm_fwd(const float* x, const float* gamma, const float* beta,
                            float* y, float* mean, float* rstd, int M, int C, float eps,
@@ -283,7 +283,8 @@ bt_status bt_layernorm_fwd(const float* x, const float* gamma, const float* beta
  *   dbeta  = param_beta * dbeta  + sum_m dy
  * dx_beta, param_beta in {0, 1}.  dx may alias dy only when dx_beta == 0.
  * ws holds bt_layernorm_bwd_ws_bytes(M, C) bytes (per-block column partials,
- * reduced in a fixed order).
+ * reduced in a fixed order).  M = 0 (no rows): dx is not written and the
+ * parameter gradients become param_beta times themselves (zeros at 0).
  */
 bt_status bt_layernorm_bwd(const float* dy, const float* x, const float* gamma,
                            const float* mean, const float* rstd, float* dx, float* dgamma,
@@ -295,7 +296,7 @@ size_t bt_layernorm_bwd_ws_bytes(int M, int C);
  * tanh-form GELU (GPT-2 figure: GELU feed-forward sublayer; appendix "GELU
  * Forward / Backward"):  gelu(x) = x/2 (1 + tanh(sqrt(2/pi)(x + 0.044715 x^3))).
  * bt_gelu_fwd: y = gelu(x).  bt_gelu_bwd: dx = dy * gelu'(x); dx may alias dy.
- * n must be a multiple of 4.
+ * n must be a multiple of 4; n = 0 writes nothing.
  */
 bt_status bt_gelu_fwd(const float* x, float* y, size_t n, void* stream);
 bt_status bt_gelu_bwd(const float* x, const float* dy, float* dx, size_t n, void* stream);
@@ -306,7 +307,8 @@ bt_status bt_gelu_bwd(const float* x, const float* dy, float* dx, size_t n, void
  * of the forward against the target; appendix "Sparse Cross-Entropy Loss").
  *   lse[m]       = log sum_{j<V} exp(z[m, j])
  *   loss_rows[m] = lse[m] - z[m, targets[m]]
- * targets in [0, V).  Vp multiple of 4, V <= Vp.  The targets live on the
+ * targets in [0, V).  Vp multiple of 4, V <= Vp, M >= 0 (M = 0 writes
+ * nothing, in all three calls).  The targets live on the
  * device and are not checked on the host: a row whose target lies outside
  * [0, V) gets a NaN loss and (in the backward and fused calls) a NaN gradient
  * in its columns < V, so that a training step over it reports a non-finite
@@ -332,7 +334,8 @@ bt_status bt_softmax_xent_fused(float* logits, const int32_t* targets, float* lo
  *   p = p - lr*wd*d*p - lr * (m / (1-b1^t)) / (sqrt(v / (1-b2^t)) + eps)
  * If *grad_scale is not finite, nothing is written (p, m, v keep their
  * values): a non-finite gradient norm skips the step.
- * t >= 1.  n and n_decay multiples of 4, n_decay <= n.  The scalars are
+ * t >= 1.  n and n_decay multiples of 4, n_decay <= n (n = 0 writes
+ * nothing).  The scalars are
  * host doubles: 1 - beta and the bias corrections are formed in double and
  * rounded to FP32 once (0.999 itself is not an FP32 number; 1 - 0.999f would
  * be off by 1.3e-5 relative).
@@ -348,7 +351,7 @@ bt_status bt_adamw_step(float* p, const float* g, float* m, float* v, size_t n, 
  * without clipping, so that bt_adamw_step given this coefficient skips the
  * update.  Writes the two device scalars out_norm[0], out_coef[0].
  * Fixed-order two-stage reduction.  ws holds bt_grad_norm_ws_bytes(n) bytes.
- * n multiple of 4.
+ * n multiple of 4; n = 0 is an empty sum (norm 0).
  */
 bt_status bt_grad_norm_clip(const float* g, size_t n, float clip, float* out_norm,
                             float* out_coef, void* ws, size_t ws_bytes, void* stream);
@@ -357,8 +360,10 @@ size_t bt_grad_norm_ws_bytes(size_t n);
 /*
  * Embeddings with learned positions and the token table tied to the LM head
  * (GPT-2 architecture figure).  tokens [B, T] int32 (values outside [0, Vp)
- * are clamped to that range).  C a multiple of 4, 0 < Vp <= 2^24,
- * B*T*C/4 < 2^31; otherwise BT_ESHAPE.
+ * are clamped to that range).  C a multiple of 4, 0 < Vp <= 2^24, B, T >= 0,
+ * B*T*C/4 < 2^31; otherwise BT_ESHAPE.  With B*T = 0 there are no
+ * positions: x0 and dwte are not written, and the rows t < T of dwpe become
+ * wpe_beta * dwpe (zeros at wpe_beta = 0).
  * fwd: x0[b, t, :] = wte[tokens[b, t], :] + wpe[t, :]            (x0 [B*T, C])
  * bwd: dwte[v, :] += sum over positions with token v of dx0       (always accumulates)
  *      dwpe[t, :]  = wpe_beta * dwpe[t, :] + sum_b dx0[b, t, :]    (rows t < T; wpe_beta 0 or 1)
@@ -399,6 +404,7 @@ size_t bt_embedding_bwd_indexed_ws_bytes(int B, int T, int C);
  * Column sums ("reduce-sum" kernel of the appendix; bias gradients):
  *   out[n] = beta * out[n] + sum_m X[m, n]      (X [M, N], ldx >= N)
  * Fixed-order two-stage reduction.  ws holds bt_colsum_ws_bytes(M, N) bytes.
+ * M >= 0: with no rows, out becomes beta * out (zeros at beta = 0).
  */
 bt_status bt_colsum(const float* X, int M, int N, int ldx, float* out, float beta, void* ws,
                     size_t ws_bytes, void* stream);

@@ -701,6 +701,15 @@ bt_status launch_bwd(const void* index, const float* dx0, float* dwte, float* dw
 
 }  // namespace
 
+// A backward over no positions (B = 0 or T = 0): no dwte row gets anything,
+// and the rows t < T of dwpe get an empty batch sum, so they become
+// wpe_beta * dwpe (zeros at wpe_beta = 0).
+static bt_status bwd_no_positions(float* dwpe, float wpe_beta, int T, int C, const char* who, hipStream_t s) {
+  if (T == 0 || wpe_beta != 0.f) return BT_OK;
+  BT_RETURN_IF(!dwpe, BT_EINVAL, "%s: NULL pointer", who);
+  return fill_zero(dwpe, (size_t)T * C, s);
+}
+
 // Internal entry points of the composed step (bt_internal.h).
 size_t emb_index_bytes(long long M) { return M > 0 ? index_layout(M).total : 0; }
 size_t emb_bwd_partials_bytes(long long M, int C) { return M > 0 ? partials_bytes(M, C) : 0; }
@@ -752,7 +761,7 @@ extern "C" bt_status bt_embedding_bwd_indexed(const void* index, size_t index_by
   bt::clear_error();
   BT_TRY(check_shape(B, T, C, Vp, "bt_embedding_bwd_indexed"));
   BT_RETURN_IF(wpe_beta != 0.f && wpe_beta != 1.f, BT_EINVAL, "bt_embedding_bwd_indexed: wpe_beta must be 0 or 1");
-  if (B * T == 0) return BT_OK;
+  if (B * T == 0) return bwd_no_positions(dwpe, wpe_beta, T, C, "bt_embedding_bwd_indexed", as_stream(stream));
   BT_RETURN_IF(!index || !dx0 || !dwte || !dwpe, BT_EINVAL, "bt_embedding_bwd_indexed: NULL pointer");
   BT_RETURN_IF(index_bytes < bt_embedding_index_bytes(B, T), BT_EWORKSPACE,
                "bt_embedding_bwd_indexed: index of %zu bytes needed (got %zu)", bt_embedding_index_bytes(B, T),
@@ -780,7 +789,7 @@ extern "C" bt_status bt_embedding_bwd(const int32_t* tokens, const float* dx0, f
   BT_TRY(check_shape(B, T, C, Vp, "bt_embedding_bwd"));
   BT_RETURN_IF(wpe_beta != 0.f && wpe_beta != 1.f, BT_EINVAL, "bt_embedding_bwd: wpe_beta must be 0 or 1");
   const int M = B * T;
-  if (M == 0) return BT_OK;
+  if (M == 0) return bwd_no_positions(dwpe, wpe_beta, T, C, "bt_embedding_bwd", as_stream(stream));
   BT_RETURN_IF(!tokens || !dx0 || !dwte || !dwpe, BT_EINVAL, "bt_embedding_bwd: NULL pointer");
   BT_RETURN_IF(!aligned16(dx0) || !aligned16(dwte) || !aligned16(dwpe), BT_EALIGN,
                "bt_embedding_bwd: float tensors must be 16-byte aligned");
