@@ -101,6 +101,10 @@ def test_other_validation(lib):
     assert lib.bt_layernorm_fwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 4, 8, 1e-5, None) == BT_EINVAL  # y aliases x
     assert lib.bt_layernorm_bwd(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1.0, 0.0, None, 0, 4, 8, None) == BT_EINVAL
     assert lib.bt_softmax_xent_fwd(FAKE, FAKE, FAKE, FAKE, 4, 10, 8, None) == BT_ESHAPE
+    # the widest row the cross-entropy kernels take is 65,536 columns
+    assert lib.bt_softmax_xent_fwd(FAKE, FAKE, FAKE, FAKE, 4, 65537, 65540, None) == BT_ESHAPE
+    assert lib.bt_softmax_xent_fused(FAKE, FAKE, FAKE, FAKE, 1.0, 4, 65537, 65540, None) == BT_ESHAPE
+    assert lib.bt_layernorm_fwd(FAKE, FAKE, FAKE, FAKE + 64, FAKE, FAKE, 4, 4100, 1e-5, None) == BT_ESHAPE
     assert lib.bt_adamw_step(FAKE, FAKE, FAKE, FAKE, 8, 4, 1e-3, 0.9, 0.95, 1e-8, 0.1, 0, None, None) == BT_EINVAL
     assert lib.bt_adamw_step(FAKE, FAKE, FAKE, FAKE, 8, 12, 1e-3, 0.9, 0.95, 1e-8, 0.1, 1, None, None) == BT_ESHAPE
     assert lib.bt_gelu_fwd(FAKE, FAKE, 6, None) == BT_ESHAPE

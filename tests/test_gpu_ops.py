@@ -21,8 +21,10 @@ RNG = np.random.Generator(np.random.PCG64(4))
 
 
 # ------------------------------------------------------------------ LayerNorm
+# Row widths of 1, 2, 3, 4, 6, 8, 12 and 16 float4 per lane (each register
+# case of the kernels; 4096 is the largest C), ragged row counts.
 @pytest.mark.parametrize("M,C", [(1, 64), (37, 768), (16384, 768), (5, 4096), (9, 1000), (2048, 3072),
-                                 (300, 2600)])
+                                 (300, 2600), (33, 400), (17, 1300), (13, 1800), (9, 3500)])
 def test_layernorm(M, C):
     torch = torch_gpu()
     say(f"layernorm M={M} C={C}")
@@ -68,7 +70,11 @@ def test_gelu(n):
 
 
 # --------------------------------------------------------------- Cross-entropy
-@pytest.mark.parametrize("M,V,Vp", [(5, 256, 256), (7, 50257, 50304), (3, 13, 16), (2, 1, 4)])
+# Vocabularies of 1, 2, 4, 8, 13 and 16 float4 per thread of the row kernel
+# (the last at the largest supported Vp, 65,536), ragged V < Vp.
+@pytest.mark.parametrize("M,V,Vp", [(5, 256, 256), (7, 50257, 50304), (3, 13, 16), (2, 1, 4),
+                                    (3, 8189, 8192), (4, 16381, 16384), (3, 32765, 32768),
+                                    (2, 65533, 65536)])
 def test_xent(M, V, Vp):
     torch = torch_gpu()
     say(f"xent M={M} V={V} Vp={Vp}")
@@ -193,7 +199,10 @@ def test_grad_norm_full_arena():
 
 
 # ----------------------------------------------------------------- Embeddings
-@pytest.mark.parametrize("B,T,C,Vp,V", [(2, 32, 64, 256, 256), (16, 1024, 768, 50304, 50257), (3, 7, 12, 20, 17)])
+# The gather's register cases: rows of 1, 2, 3, 4, 6, 8 and 16 float4 per lane.
+@pytest.mark.parametrize("B,T,C,Vp,V", [(2, 32, 64, 256, 256), (16, 1024, 768, 50304, 50257), (3, 7, 12, 20, 17),
+                                        (2, 33, 400, 300, 290), (3, 17, 1000, 100, 97), (2, 9, 1300, 64, 60),
+                                        (2, 5, 1800, 64, 64), (2, 3, 4096, 16, 16)])
 def test_embedding(B, T, C, Vp, V):
     torch = torch_gpu()
     say(f"embedding B={B} T={T} C={C}")
