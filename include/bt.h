@@ -100,6 +100,16 @@ bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K,
                   const float* residual, float* colsum_B, void* ws, size_t ws_bytes,
                   void* stream);
 size_t bt_gemm_ws_bytes(bt_op opA, bt_op opB, int M, int N, int K, bt_epi epi);
+/* The launch plan bt_gemm uses for a product, computed on the host (no
+ * device work): *tile_depth, the k-depth of its 128 x 128 block tile (16 or
+ * 32); *splits, the number of K ranges whose partial products are summed in
+ * a fixed order (1 = not split; bt_gemm_ws_bytes() > 0 exactly when > 1);
+ * *direct, 1 when its operand tiles are copied straight into LDS (every tile
+ * full), 0 when they are staged with bounds checks.  The plan depends only on
+ * (opA, opB, M, N, K) and the leading dimensions, not on the epilogue.
+ * M, N, K positive multiples of 4, else BT_ESHAPE; NULL outputs BT_EINVAL. */
+bt_status bt_gemm_plan(bt_op opA, bt_op opB, int M, int N, int K, int lda, int ldb, int* tile_depth,
+                       int* splits, int* direct);
 
 /*
  * bt_gemm for callers that cannot allocate device memory: code under HIP

@@ -89,6 +89,7 @@ _SIGS = {
     "bt_version": (_c.c_char_p, []),
     "bt_gemm": (i32, [i32, i32, i32, i32, i32, vp, i32, vp, i32, f32, vp, i32, vp, i32, vp, vp, vp, vp, vp, sz, vp]),
     "bt_gemm_ws_bytes": (sz, [i32, i32, i32, i32, i32, i32]),
+    "bt_gemm_plan": (i32, [i32, i32, i32, i32, i32, i32, i32, _c.POINTER(i32), _c.POINTER(i32), _c.POINTER(i32)]),
     "bt_gemm_noalloc": (i32, [i32, i32, i32, i32, i32, vp, i32, vp, i32, f32, vp, i32, vp, i32, vp, vp, vp, vp, vp]),
     "bt_gemm_noalloc_max_ws_bytes": (sz, []),
     "bt_attention_fwd": (i32, [vp, vp, vp, i32, i32, i32, i32, vp]),
@@ -216,6 +217,14 @@ def bt_gemm(opA, opB, M, N, K, A, lda, B, ldb, beta, C, ldc, bias=None, epi=EPI_
                      _p(preact_out), _p(gelu_in), _p(residual), _p(colsum_B), _p(w), nbytes,
                      _stream(stream)), "bt_gemm")
     return C
+
+
+def bt_gemm_plan(opA, opB, M, N, K, lda, ldb):
+    """(tile_depth, splits, direct) of the launch bt_gemm makes for the product."""
+    d, sp, dr = i32(0), i32(0), i32(0)
+    _check(lib().bt_gemm_plan(opA, opB, M, N, K, lda, ldb, _c.byref(d), _c.byref(sp), _c.byref(dr)),
+           "bt_gemm_plan")
+    return d.value, sp.value, dr.value
 
 
 def bt_gemm_noalloc(opA, opB, M, N, K, A, lda, B, ldb, beta, C, ldc, bias=None, epi=EPI_NONE,

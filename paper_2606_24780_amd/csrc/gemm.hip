@@ -770,6 +770,10 @@ GemmCfg choose_config(int M, int N, int K, bool akc, bool bkc, bool may_split) {
   // with more resident blocks, then the smaller split
   for (int tc = NUM_TILE_CFGS - 1; tc >= 0; --tc) {
     if (deep_only && kTileCfgs[tc].bk != 32) continue;
+    // with both operands MN-contiguous the 32-deep tile is slower at every
+    // block count (its rate_mn and per-block cost are both worse); it is not
+    // built for that layout
+    if (!akc && !bkc && kTileCfgs[tc].bk != 16) continue;
     const TileCfg& c = kTileCfgs[tc];
     const int bm = 32 * c.mb * c.wm, bn = 32 * c.nb * c.wn, bk = c.bk;
     const long long tiles = (long long)((M + bm - 1) / bm) * ((N + bn - 1) / bn);
@@ -831,10 +835,13 @@ void launch_layout(const GemmParams& p, const GemmCfg& c, int epi, bool split, b
 #define BT_GEMM_CFG(BK_, OCC_, WM_, WN_, MB_, NB_)                                         \
   if (dtl) launch_cfg<A_KC, B_KC, BK_, OCC_, WM_, WN_, MB_, NB_, true>(p, epi, split, grid, s); \
   else launch_cfg<A_KC, B_KC, BK_, OCC_, WM_, WN_, MB_, NB_, false>(p, epi, split, grid, s)
-  switch (c.tc) {
-    case 0: BT_GEMM_CFG(32, 2, 2, 2, 2, 2); break;
-    default: BT_GEMM_CFG(16, 4, 2, 2, 2, 2); break;
+  if constexpr (A_KC || B_KC) {
+    if (c.tc == 0) {
+      BT_GEMM_CFG(32, 2, 2, 2, 2, 2);
+      return;
+    }
   }
+  BT_GEMM_CFG(16, 4, 2, 2, 2, 2);
 #undef BT_GEMM_CFG
 }
 
@@ -934,6 +941,32 @@ bt_status gemm_segmented_batched(int M, int N, int K, const float* A, int lda, l
 
 using namespace bt;
 
+namespace bt {
+namespace {
+// Direct global-to-LDS operand copies: every tile of the launch is full and
+// the per-lane copy offsets fit their 32-bit registers.
+bool direct_tiles(const GemmCfg& cfg, int M, int N, int K, int lda, int ldb) {
+  const TileCfg& t = kTileCfgs[cfg.tc];
+  return M % (32 * t.mb * t.wm) == 0 && N % (32 * t.nb * t.wn) == 0 && K % t.bk == 0 && copy_offsets_fit(lda, ldb);
+}
+}  // namespace
+}  // namespace bt
+
+extern "C" bt_status bt_gemm_plan(bt_op opA, bt_op opB, int M, int N, int K, int lda, int ldb, int* tile_depth,
+                                  int* splits, int* direct) {
+  bt::clear_error();
+  BT_RETURN_IF(opA != BT_OP_N && opA != BT_OP_T, BT_EINVAL, "bt_gemm_plan: bad opA %d", (int)opA);
+  BT_RETURN_IF(opB != BT_OP_N && opB != BT_OP_T, BT_EINVAL, "bt_gemm_plan: bad opB %d", (int)opB);
+  BT_RETURN_IF(M <= 0 || N <= 0 || K <= 0 || ((M | N | K) & 3), BT_ESHAPE,
+               "bt_gemm_plan: M=%d N=%d K=%d must be positive multiples of 4", M, N, K);
+  BT_RETURN_IF(!tile_depth || !splits || !direct, BT_EINVAL, "bt_gemm_plan: NULL output");
+  const GemmCfg c = choose_config(M, N, K, opA == BT_OP_N, opB == BT_OP_T, true);
+  *tile_depth = kTileCfgs[c.tc].bk;
+  *splits = c.splits;
+  *direct = direct_tiles(c, M, N, K, lda, ldb) ? 1 : 0;
+  return BT_OK;
+}
+
 extern "C" size_t bt_gemm_ws_bytes(bt_op opA, bt_op opB, int M, int N, int K, bt_epi epi) {
   if (M <= 0 || N <= 0 || K <= 0 || epi < BT_EPI_NONE || epi > BT_EPI_DGELU) return 0;
   const GemmCfg c = choose_config(M, N, K, opA == BT_OP_N, opB == BT_OP_T, true);
@@ -1012,8 +1045,7 @@ extern "C" bt_status bt_gemm(bt_op opA, bt_op opB, int M, int N, int K, const fl
   BT_RETURN_IF(nblocks > 0x7fffffffLL, BT_ESHAPE, "bt_gemm: too many tiles");
   dim3 grid((unsigned)nblocks);
   hipStream_t s = as_stream(stream);
-  const int bk = kTileCfgs[cfg.tc].bk;
-  const bool dtl = M % bm == 0 && N % bn == 0 && K % bk == 0 && copy_offsets_fit(lda, ldb);
+  const bool dtl = direct_tiles(cfg, M, N, K, lda, ldb);
   if (akc && !bkc) launch_layout<true, false>(p, cfg, epi, split, dtl, grid, s);
   else if (akc && bkc) launch_layout<true, true>(p, cfg, epi, split, dtl, grid, s);
   else if (!akc && !bkc) launch_layout<false, false>(p, cfg, epi, split, dtl, grid, s);

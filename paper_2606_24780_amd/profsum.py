@@ -16,8 +16,12 @@
         dispatch), scaled by what the same counters read for a plain 1 GiB copy:
         the GEMM class's bytes per bt_gemm call (JSON read by bench.py) and the
         memory-bound kernels' measured bytes against their algorithmic bytes.
+    python -m paper_2606_24780_amd.profsum coverage LIBBT_SO STATS_CSV [--command CMD ...]
+        which kernel instantiations of the built library a traced run (e.g. the
+        GPU test suite under rocprofv3 --kernel-trace --stats) launched.
 
-Reads only CSV files that rocprofv3 wrote; runs nothing on the GPU.
+Reads the CSV files that rocprofv3 wrote (and, for coverage, the symbol
+table of the library built here, through nm); runs nothing on the GPU.
 """
 from __future__ import annotations
 
@@ -374,6 +378,48 @@ def mode_markdown(bench_json, stats_csv, commands=None):
     return "\n".join(out) + "\n"
 
 
+def _plain_kernel_name(name):
+    name = name.strip()
+    return name[5:] if name.startswith("void ") else name
+
+
+def library_kernels(lib_path):
+    """The __global__ functions of a library built here: HIP gives each one a
+    host-side handle, a data symbol named like the kernel (demangled, a
+    function signature)."""
+    import subprocess
+    out = subprocess.run(["nm", "-C", lib_path], capture_output=True, text=True, check=True).stdout
+    names = set()
+    for ln in out.splitlines():
+        parts = ln.split(" ", 2)
+        if len(parts) == 3 and parts[1] in ("d", "D") and parts[2].rstrip().endswith(")"):
+            names.add(_plain_kernel_name(parts[2]))
+    return names
+
+
+def coverage_markdown(lib_path, stats_csv, commands=None):
+    """Kernel instantiations of the library launched / never launched by the
+    traced run, per kernel family."""
+    built = library_kernels(lib_path)
+    launched = {_plain_kernel_name(r["name"]) for r in read_stats(stats_csv)}
+    family = lambda n: re.split(r"[<(]", n.replace("(anonymous namespace)::", ""))[0].split("::")[-1]
+    fams = defaultdict(lambda: [0, 0])
+    for n in built:
+        fams[family(n)][0] += 1
+        fams[family(n)][1] += n in launched
+    missing = sorted(n for n in built if n not in launched)
+    out = []
+    if commands:
+        out += ["Commands (run from the repository root):", "", "```", *commands, "```", ""]
+    out += [f"{len(built)} kernel instantiations in the library; {len(built) - len(missing)} launched by the traced "
+            f"run, {len(missing)} not.", "", "| kernel | instantiations | launched |", "|---|---:|---:|"]
+    for f, (nb, nl) in sorted(fams.items()):
+        out.append(f"| `{f}` | {nb} | {nl} |")
+    if missing:
+        out += ["", "Not launched:", ""] + [f"- `{n}`" for n in missing]
+    return "\n".join(out) + "\n"
+
+
 def main():
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -406,8 +452,14 @@ def main():
     r.add_argument("full", type=float)
     r.add_argument("steps", type=int)
     r.add_argument("--command")
+    cv = sub.add_parser("coverage")
+    cv.add_argument("lib")
+    cv.add_argument("stats")
+    cv.add_argument("--command", action="append")
     a = ap.parse_args()
-    if a.cmd == "mode":
+    if a.cmd == "coverage":
+        print(coverage_markdown(a.lib, a.stats, a.command), end="")
+    elif a.cmd == "mode":
         print(mode_markdown(a.bench_json, a.stats, a.command), end="")
     elif a.cmd == "ratio":
         print(ratio_markdown(a.csv, a.num, a.den, a.full, a.steps, a.command), end="")

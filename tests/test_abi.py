@@ -113,6 +113,31 @@ def test_other_validation(lib):
     assert lib.bt_grad_norm_clip(FAKE, 8, 1.0, None, None, None, 0, None) == BT_EINVAL
 
 
+def test_gemm_plan(lib):
+    """bt_gemm_plan (host only) agrees with the workspace query (split exactly
+    when a workspace is needed), takes the 32-deep tile for the LM head's
+    input gradient (K = 50,304 over 768 tiles) and never for products with
+    both operands MN-contiguous, copies full tiles directly and stages ragged
+    ones, and validates its arguments."""
+    shapes = [(0, 0, 16384, 768, 50304), (0, 1, 16384, 50304, 768), (1, 0, 768, 50304, 16384),
+              (0, 0, 16384, 2304, 768), (1, 0, 768, 2304, 16384), (0, 0, 260, 196, 132), (1, 1, 4, 4, 4),
+              (0, 1, 16384, 768, 3072), (1, 1, 1028, 2052, 8196)]
+    for ta, tb, M, N, K in shapes:
+        d, sp, dr = bt.bt_gemm_plan(ta, tb, M, N, K, M if ta else K, K if tb else N)
+        assert d in (16, 32) and sp >= 1 and dr in (0, 1)
+        assert (sp > 1) == (lib.bt_gemm_ws_bytes(ta, tb, M, N, K, 0) > 0)
+        ragged = M % 128 or N % 128 or K % d
+        assert dr == (0 if ragged else 1)
+    assert bt.bt_gemm_plan(0, 0, 16384, 768, 50304, 50304, 768)[0] == 32
+    for M, N, K in [(768, 50304, 16384), (4096, 2048, 32768), (2048, 4096, 1024), (384, 2048, 4096)]:
+        assert bt.bt_gemm_plan(1, 0, M, N, K, M, N)[0] == 16
+    with pytest.raises(bt.BTError) as e:
+        bt.bt_gemm_plan(0, 0, 6, 4, 4, 4, 4)
+    assert e.value.status == BT_ESHAPE
+    d = ctypes.c_int()
+    assert lib.bt_gemm_plan(0, 0, 4, 4, 4, 4, 4, ctypes.byref(d), None, ctypes.byref(d)) == BT_EINVAL
+
+
 def test_attention_workspace_sizes(lib):
     """Row sums D always; the stored-dS method adds B H T T floats when T % 4 == 0."""
     def al(x):

@@ -97,3 +97,28 @@ def test_mode_markdown(tmp_path):
     md = profsum.mode_markdown(str(bench), str(stats), ["cmd"])
     assert "| kernel | median_ms | gbs |" in md and "| b | 1.0 | 3.0 |" in md
     assert "50.0%" in md and "| `k1` | 2 | 2.0 | 80.0 |" in md
+
+
+def test_coverage_markdown(tmp_path):
+    """Kernel instantiations of the built library (its host-side kernel
+    handles) against the kernels a traced run launched."""
+    import os
+    import pytest
+    lib = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2606_24780_amd",
+                       "libbt.so")
+    if not os.path.exists(lib):
+        pytest.skip("library not built")
+    built = profsum.library_kernels(lib)
+    assert "bt::fill_zero_kernel(float*, unsigned long)" in built
+    assert sum("gemm_f32_mfma<" in n for n in built) > 40
+    assert not any(n.startswith("void ") for n in built)
+    picked = sorted(built)[:3]
+    stats = tmp_path / "s.csv"
+    _write(stats, ["Name", "Calls", "TotalDurationNs", "AverageNs", "Percentage", "MinNs", "MaxNs", "StdDev"],
+           [["void " + picked[0], 1, 1e3, 1e3, 50.0, 1, 1, 0], [picked[1], 2, 1e3, 5e2, 40.0, 1, 1, 0],
+            [picked[2], 1, 1e2, 1e2, 5.0, 1, 1, 0], ["__amd_rocclr_copyBuffer", 4, 1e2, 25, 5.0, 1, 1, 0]])
+    md = profsum.coverage_markdown(lib, str(stats), ["cmd"])
+    assert f"{len(built)} kernel instantiations in the library; 3 launched by the traced run, " \
+           f"{len(built) - 3} not." in md
+    assert f"- `{picked[0]}`" not in md and f"- `{sorted(built)[3]}`" in md
+    assert "| `fill_zero_kernel` | 1 |" in md
