@@ -103,10 +103,14 @@ def test_block_fwd_single_segments_unaligned_to_tiles():
         _check_block(host(out).reshape(B, seg, H, hd), host(lse), r_out, r_lse, f"q{qp} k{kp}")
 
 
+# The last two: shards of 8448 rows, above the 8192 where the stored-dS dQ
+# product takes its long-shard tile (head dim 64: direct tiles; 48: staged).
 @pytest.mark.parametrize("B,T,W,H,hd,pairs", [
     (2, 1024, 2, 2, 64, [(0, 0), (0, 1), (1, 0)]),
     (1, 2048, 4, 2, 32, [(0, 3), (3, 0), (2, 2)]),
     (1, 1024, 2, 2, 128, [(1, 0), (1, 1)]),
+    (1, 16896, 2, 1, 64, [(1, 0)]),
+    (1, 16896, 2, 1, 48, [(0, 0)]),
 ])
 @pytest.mark.parametrize("stored", [False, True])
 def test_block_bwd_vs_oracle(B, T, W, H, hd, pairs, stored):
