@@ -2,7 +2,9 @@
 
 * fourth-order central finite differences of the loss on the tiny model:
   >= 32 sampled entries of every tensor plus every entry of one LN gain;
-* an independent torch-CPU float64 autograd model of the same definitions;
+* an independent torch-CPU float64 autograd model of the same definitions
+  (tiny model, padded vocabulary, and the GPT-2 124M shapes on a short
+  sequence);
 * loss = ln(V) exactly when the token embedding is zero (tiny and 124M shapes);
 * 4 micro-steps of B/4 equal one step of B in exact arithmetic;
 * one-block forward/backward against torch autograd.
@@ -117,6 +119,27 @@ def test_padded_vocab_model_vs_torch(torch_cpu):
     for name in grads:
         assert np.allclose(grads[name], tg[name], rtol=1e-9, atol=1e-14), name
     # padded rows of the tied embedding receive exactly zero gradient
+    assert np.all(grads["wte"][cfg.V:] == 0)
+
+
+@pytest.mark.slow
+def test_124m_model_vs_torch_autograd(torch_cpu):
+    """The oracle's forward and backward at the GPT-2 124M shapes (12 layers,
+    768 wide, 12 heads, vocabulary 50,257 padded to 50,304) on one 16-token
+    sequence, every 1-D parameter perturbed so that no term vanishes."""
+    cfg = synth.GPT2_124M
+    params = synth.init_params(cfg, 9)
+    rng = np.random.Generator(np.random.PCG64(10))
+    for k in params:
+        if params[k].ndim == 1:
+            params[k] = params[k] + 0.05 * rng.standard_normal(params[k].shape).astype(np.float32)
+    stream = synth.zipf_tokens(16 + 1, cfg.V, 1.1, 41)
+    x, y = synth.shifted_pair(stream, 1, 16)
+    loss, _, grads = og.fwd_bwd(cfg, params, x, y)
+    tl, tg = _torch_model(torch_cpu, cfg, params, x, y)
+    assert abs(loss - tl) < 1e-12 * abs(tl)
+    for name in grads:
+        assert np.allclose(grads[name], tg[name], rtol=1e-9, atol=1e-13 * max(1, np.abs(tg[name]).max())), name
     assert np.all(grads["wte"][cfg.V:] == 0)
 
 
