@@ -246,6 +246,48 @@ def test_deep_narrow_accumulation_vs_oracle():
                   what="deep accum")
 
 
+@pytest.mark.parametrize("B,T", [(3, 100), (4, 37)])
+def test_ragged_step_vs_oracle(B, T):
+    """The composed step at a sequence length below the model's maximum and a
+    multiple of no tile.  The model is narrow: C = 96, three heads of 32, and
+    a vocabulary of 300 padded to 304.  M = B*T = 300 uses the stored-dS
+    attention backward.  With T = 37 (not a multiple of 4) the backward
+    recomputes instead.  Loss, every gradient and the clipped AdamW update
+    are checked against the oracle.  The gradient buffer starts filled with a
+    sentinel, and the step must overwrite all of it: the rows of wpe beyond T
+    and the padded rows of wte come out exactly zero."""
+    torch = torch_gpu()
+    cfg = synth.GPT2Config(V=300, Vp=304, max_T=128, L=2, H=3, C=96)
+    hp = synth.HP_124M
+    specs = synth.param_specs(cfg)
+    params = synth.init_params(cfg, 12)
+    rng = np.random.Generator(np.random.PCG64(120))
+    for name in params:
+        if name.endswith(("ln1g", "ln2g", "lnfg")):
+            params[name] = (1.0 + 0.2 * rng.standard_normal(params[name].shape)).astype(np.float32)
+        elif params[name].ndim == 1:
+            params[name] = (0.2 * rng.standard_normal(params[name].shape)).astype(np.float32)
+    stream = synth.zipf_tokens(B * T + 1, cfg.V, 1.1, 13)
+    x, y = synth.shifted_pair(stream, B, T)
+    say(f"gpt2 ragged step B={B} T={T} (max_T={cfg.max_T}, Vp={cfg.Vp})")
+    model = bt.GPT2(cfg, hp, B, T)
+    model.load_params(synth.flatten(cfg, params))
+    model.grads.fill_(7.25)  # a step that does not accumulate writes every gradient element
+    loss = model.train_step(dev(torch, x), dev(torch, y))
+    torch.cuda.synchronize()
+    zeros = {k: np.zeros_like(v, dtype=np.float64) for k, v in params.items()}
+    ref = og.train_step(cfg, hp, specs, params, zeros, zeros, x, y, t=1)
+    say(f"loss gpu={loss:.8f} oracle={ref['loss']:.8f}")
+    assert abs(loss - ref["loss"]) <= LOSS_TOL * abs(ref["loss"])
+    g = _unflat(cfg, model.grads)
+    for name, _, _ in specs:
+        assert_close_maxabs(g[name], ref["grads"][name], GRAD_TOL, f"grad {name}")
+    assert np.all(g["wte"][cfg.V:] == 0) and np.all(g["wpe"][T:] == 0)
+    p, m, v = _unflat(cfg, model.params), _unflat(cfg, model.m), _unflat(cfg, model.v)
+    norm, coef = _check_update(cfg, hp, specs, params, g, p, m, v, 1, what="ragged")
+    _check_end_to_end(hp, specs, params, g, ref["grads"], p, ref["params"], c_gpu=coef, c_or=ref["coef"])
+
+
 # ---------------------------------------------------------------- GPT-2 124M
 def _inputs_124m(B=16, T=1024):
     cfg = synth.GPT2_124M
