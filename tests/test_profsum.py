@@ -108,6 +108,9 @@ def test_coverage_markdown(tmp_path):
                        "libbt.so")
     if not os.path.exists(lib):
         pytest.skip("library not built")
+    import shutil
+    if shutil.which("nm") is None:
+        pytest.skip("nm (binutils) not installed")
     built = profsum.library_kernels(lib)
     assert "bt::fill_zero_kernel(float*, unsigned long)" in built
     assert sum("gemm_f32_mfma<" in n for n in built) > 40
